@@ -1,0 +1,258 @@
+/*
+ * lacache_oracle.c -- plain CPU oracle for the LaCache two-stage cache lookup.
+ *
+ * TEST INFRASTRUCTURE ONLY.  The product library never links, loads or calls
+ * this file; only the test-suite, the smoke check and the benchmark's CPU
+ * baseline do.  It shares no code, header, table or helper with the HIP path.
+ *
+ * Everything here is computed in IEEE double, slowly and in the most direct
+ * order, so that it can be checked against the paper by eye:
+ *
+ *   quantise  Cosine similarity (Section 3: the distance between embeddings is
+ *             e.g. cosine distance; Section 5.1: a hit needs sim >= tau) is the
+ *             dot product of L2-normalised vectors.  A vector is normalised in
+ *             double and rounded ONCE, to nearest-even, to bfloat16 -- the
+ *             precision the cache stores.  A zero vector stays zero.
+ *   stage 1   The cached entry whose key has the largest dot product with the
+ *             query (lowest index on exact ties) is "the hit" candidate
+ *             (Algorithm 1: search the cache with h(x)); it is a hit when the
+ *             score, clamped to [-1, 1], is >= tau_q (Section 5.1, cache check
+ *             sim(x, x') >= tau_c).
+ *   stage 2   Run only for a stage-1 hit (Algorithm 1: the lookahead check sits
+ *             inside the hit branch).  The matched entry stores the lookahead
+ *             key of its own response prefix (Section 4.2, cache structure
+ *             <h(x), [h(f_k(x)), f(x)]>): here the first k token IDs and the
+ *             embedding of that prefix.  The lookahead passes when the k tokens
+ *             are identical (a deterministic hash of identical input always
+ *             agrees) or when the prefix-embedding cosine is >= tau_r
+ *             (Section 5.1, lookahead check sim(f_k(x), f_k(x')) >= tau_a).
+ *
+ * Decision codes: 0 MISS, 1 REJECT (collision detected), 2 HIT, 3 HIT_EXACT.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+#define LCO_MISS 0
+#define LCO_REJECT 1
+#define LCO_HIT 2
+#define LCO_HIT_EXACT 3
+
+static float quiet_nan(void)
+{
+    uint32_t u = 0x7FC00000u;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return f;
+}
+
+/* bfloat16 bit pattern -> the exact double it denotes. */
+static double widen_bf16(uint16_t h)
+{
+    uint32_t u = (uint32_t)h << 16;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return (double)f;
+}
+
+/*
+ * Round a double to the nearest bfloat16 (8 significant bits, 8 exponent
+ * bits), ties to even, in ONE rounding step.  The representable grid near |v|
+ * has spacing 2^(e-7) where 2^e is the leading bit of |v|; below the smallest
+ * normal binade (e < -126) the spacing stays 2^-133 (subnormals).  Scaling by
+ * a power of two is exact, so nearbyint() (default mode: to nearest, ties to
+ * even) does the only rounding.
+ */
+uint16_t lco_bf16_rne(double v)
+{
+    if (isnan(v))
+        return 0x7FC0;
+    if (isinf(v))
+        return signbit(v) ? 0xFF80 : 0x7F80;
+    if (v == 0.0)
+        return signbit(v) ? 0x8000 : 0x0000;
+    int ex;
+    frexp(fabs(v), &ex); /* |v| = m * 2^ex with m in [0.5, 1) */
+    int lead = ex - 1;   /* weight of the leading bit */
+    if (lead < -126)
+        lead = -126;
+    double r = nearbyint(ldexp(v, 7 - lead));
+    double w = ldexp(r, lead - 7);
+    if (fabs(w) >= 0x1p128)
+        return signbit(v) ? 0xFF80 : 0x7F80;
+    float f = (float)w; /* exact: at most 8 significant bits, within float range */
+    uint32_t bits;
+    memcpy(&bits, &f, sizeof bits);
+    return (uint16_t)(bits >> 16);
+}
+
+/* Element j of row r of an input matrix, as a double.  dtype 0 = float32, 1 = bfloat16. */
+static double read_in(const void *in, int32_t dtype, int64_t r, int32_t d, int32_t j)
+{
+    if (dtype == 0)
+        return (double)((const float *)in)[r * (int64_t)d + j];
+    return widen_bf16(((const uint16_t *)in)[r * (int64_t)d + j]);
+}
+
+/*
+ * L2-normalise each of `rows` rows of length d in double and round each
+ * component once to bfloat16.  A zero row gives an all-zero (+0) row.
+ * out is [rows][d] bfloat16 bit patterns.
+ */
+void lco_quantise(const void *in, int32_t dtype, int64_t rows, int32_t d, uint16_t *out)
+{
+#pragma omp parallel for schedule(static)
+    for (int64_t r = 0; r < rows; ++r) {
+        double ss = 0.0;
+        for (int32_t j = 0; j < d; ++j) {
+            double v = read_in(in, dtype, r, d, j);
+            ss += v * v;
+        }
+        double n = sqrt(ss);
+        for (int32_t j = 0; j < d; ++j) {
+            uint16_t q = 0;
+            if (n != 0.0)
+                q = lco_bf16_rne(read_in(in, dtype, r, d, j) / n);
+            out[r * (int64_t)d + j] = q;
+        }
+    }
+}
+
+/* Dot product of two bfloat16 rows, accumulated in double in index order. */
+double lco_dot(const uint16_t *x, const uint16_t *y, int32_t d)
+{
+    double s = 0.0;
+    for (int32_t j = 0; j < d; ++j)
+        s += widen_bf16(x[j]) * widen_bf16(y[j]);
+    return s;
+}
+
+static float clamp_unit(double s)
+{
+    float f = (float)s; /* one rounding to float, to nearest */
+    if (f < -1.0f)
+        f = -1.0f;
+    if (f > 1.0f)
+        f = 1.0f;
+    return f;
+}
+
+/*
+ * Steps after the top-1 search, for query b against an arbitrary entry i:
+ * stage-1 threshold, and stage 2 if it passes.  Returns the decision and
+ * writes the clamped stage-1 score and the stage-2 score (NaN if stage 2 did
+ * not run).
+ */
+static int32_t decide_one(const uint16_t *keys, const uint16_t *emb, const int32_t *tokens, int32_t d,
+                          int32_t k_cap, const uint16_t *q, const uint16_t *a, const int32_t *u,
+                          float tau_q, float tau_r, int32_t k, int64_t i, double *s_out, float *score_out,
+                          float *resp_out)
+{
+    double s = lco_dot(q, keys + i * (int64_t)d, d);
+    float score = clamp_unit(s);
+    *s_out = s;
+    *score_out = score;
+    *resp_out = quiet_nan();
+    if (!(score >= tau_q))
+        return LCO_MISS;
+    float r = clamp_unit(lco_dot(a, emb + i * (int64_t)d, d));
+    *resp_out = r;
+    int tok_eq = 1;
+    for (int32_t j = 0; j < k; ++j)
+        if (u[j] != tokens[i * (int64_t)k_cap + j])
+            tok_eq = 0;
+    if (tok_eq)
+        return LCO_HIT_EXACT;
+    return (r >= tau_r) ? LCO_HIT : LCO_REJECT;
+}
+
+/*
+ * The full two-stage lookup over quantised inputs.
+ *   keys, emb : [N][d]     quantised cache keys and response-prefix embeddings
+ *   tokens    : [N][k_cap] stored response-prefix token IDs
+ *   q, a      : [B][d]     quantised queries and lookahead embeddings
+ *   u         : [B][k]     lookahead token IDs
+ * Outputs per query: idx (argmax, -1 when N == 0), score (clamped maximum,
+ * NaN when N == 0), resp_score (NaN unless stage 2 ran), decision, and the
+ * unclamped double maximum s_best and top-2 margin (best minus the best over
+ * every other entry; +inf when N == 1, 0 for exact ties).
+ */
+void lco_lookup(const uint16_t *keys, const uint16_t *emb, const int32_t *tokens, int64_t N, int32_t d,
+                int32_t k_cap, const uint16_t *q, const uint16_t *a, const int32_t *u, int32_t B, float tau_q,
+                float tau_r, int32_t k, int32_t *idx, float *score, float *resp_score, int32_t *decision,
+                double *s_best, double *margin)
+{
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int32_t b = 0; b < B; ++b) {
+        const uint16_t *qb = q + (int64_t)b * d;
+        if (N == 0) {
+            idx[b] = -1;
+            score[b] = quiet_nan();
+            resp_score[b] = quiet_nan();
+            decision[b] = LCO_MISS;
+            s_best[b] = (double)quiet_nan();
+            margin[b] = (double)quiet_nan();
+            continue;
+        }
+        double best = -INFINITY, second = -INFINITY;
+        int64_t bi = -1;
+        for (int64_t i = 0; i < N; ++i) {
+            double s = lco_dot(qb, keys + i * (int64_t)d, d);
+            if (s > best) {
+                second = best;
+                best = s;
+                bi = i;
+            } else if (s > second) {
+                second = s;
+            }
+        }
+        idx[b] = (int32_t)bi;
+        margin[b] = best - second;
+        double s;
+        decision[b] = decide_one(keys, emb, tokens, d, k_cap, qb, a + (int64_t)b * d, u + (int64_t)b * k, tau_q,
+                                 tau_r, k, bi, &s, &score[b], &resp_score[b]);
+        s_best[b] = s;
+    }
+}
+
+/*
+ * The same post-search steps evaluated at a caller-chosen entry at[b] for
+ * each query b (used to judge a result whose index differs on a near-tie).
+ */
+void lco_decide(const uint16_t *keys, const uint16_t *emb, const int32_t *tokens, int64_t N, int32_t d,
+                int32_t k_cap, const uint16_t *q, const uint16_t *a, const int32_t *u, int32_t B, float tau_q,
+                float tau_r, int32_t k, const int32_t *at, double *s_at, float *score, float *resp_score,
+                int32_t *decision)
+{
+#pragma omp parallel for schedule(static)
+    for (int32_t b = 0; b < B; ++b) {
+        if (at[b] < 0 || at[b] >= N) {
+            s_at[b] = (double)quiet_nan();
+            score[b] = quiet_nan();
+            resp_score[b] = quiet_nan();
+            decision[b] = LCO_MISS;
+            continue;
+        }
+        decision[b] = decide_one(keys, emb, tokens, d, k_cap, q + (int64_t)b * d, a + (int64_t)b * d,
+                                 u + (int64_t)b * k, tau_q, tau_r, k, at[b], &s_at[b], &score[b], &resp_score[b]);
+    }
+}
+
+/* Lowest index j <= i whose quantised key is bitwise identical to key i. */
+int64_t lco_first_identical(const uint16_t *keys, int64_t N, int32_t d, int64_t i)
+{
+    if (i < 0 || i >= N)
+        return -1;
+    const uint16_t *ki = keys + i * (int64_t)d;
+    for (int64_t j = 0; j < i; ++j)
+        if (memcmp(keys + j * (int64_t)d, ki, (size_t)d * sizeof(uint16_t)) == 0)
+            return j;
+    return i;
+}
+
+/* Element-wise lco_bf16_rne over an array (for the tests of the rounding rule). */
+void lco_bf16_rne_array(const double *in, int64_t n, uint16_t *out)
+{
+    for (int64_t i = 0; i < n; ++i)
+        out[i] = lco_bf16_rne(in[i]);
+}

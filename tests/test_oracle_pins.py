@@ -1,0 +1,403 @@
+"""Pins of the CPU oracle against facts that do not come from the oracle itself.
+
+Each group below fixes one part of the oracle by something independent of it:
+a library routine (torch's float->bfloat16 conversion), exact rational
+arithmetic, hand-derived closed forms, a brute-force score matrix, or an
+invariant the lookup must satisfy.  Sizes keep the whole module to seconds.
+"""
+import math
+from decimal import Decimal, getcontext
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from tests import bruteforce as bf
+
+MISS, REJECT, HIT, HIT_EXACT = oracle.MISS, oracle.REJECT, oracle.HIT, oracle.HIT_EXACT
+U = 2.0 ** -8  # bfloat16 unit roundoff
+
+
+def torch_bf16(x32: np.ndarray) -> np.ndarray:
+    return torch.from_numpy(np.ascontiguousarray(x32, np.float32)).to(torch.bfloat16).view(torch.int16).numpy() \
+        .view(np.uint16)
+
+
+# --------------------------------------------------------------------------- bf16 rounding
+
+
+def test_bf16_rne_matches_torch_on_float32_values():
+    """On float32 inputs (exact in double) one rounding == torch's nearest-even float->bf16."""
+    rng = np.random.default_rng(123)
+    bits = rng.integers(0, 2 ** 32, 1_000_000, dtype=np.uint64).astype(np.uint32)
+    # force a large share of exact ties (low 16 bits == 0x8000) and near-ties
+    bits[:200_000] = (bits[:200_000] & 0xFFFF0000) | 0x8000
+    bits[200_000:250_000] = (bits[200_000:250_000] & 0xFFFF0000) | 0x7FFF
+    bits[250_000:300_000] = (bits[250_000:300_000] & 0xFFFF0000) | 0x8001
+    bits[300_000:350_000] &= 0x807FFFFF  # subnormals
+    x = bits.view(np.float32)
+    x = x[~np.isnan(x)]
+    got = oracle.bf16_rne(x.astype(np.float64))
+    want = torch_bf16(x)
+    np.testing.assert_array_equal(got, want)
+
+
+def test_bf16_rne_closed_forms():
+    cases = [
+        (1.0, 0x3F80),
+        (1 + 2 ** -8, 0x3F80),          # halfway between 1 and 1+2^-7: ties to even (down)
+        (1 + 3 * 2 ** -8, 0x3F82),      # halfway between 0x3F81 and 0x3F82: ties to even (up)
+        (1 + 2 ** -8 + 2 ** -30, 0x3F81),  # just above halfway: up.  (Rounding through float32 first
+                                           # would land exactly on the tie and go down: one rounding only.)
+        (-0.0, 0x8000),
+        (0.0, 0x0000),
+        (2.0 ** -133, 0x0001),          # smallest bf16 subnormal
+        (2.0 ** -134, 0x0000),          # half of it: tie to even (zero)
+        (1.5 * 2.0 ** -134, 0x0001),
+        (3.0e38, 0x7F62),
+        (3.4e38, 0x7F80),               # beyond the largest finite bf16 (3.3895e38) by more than half an ulp
+        (float("inf"), 0x7F80),
+        (-float("inf"), 0xFF80),
+    ]
+    got = oracle.bf16_rne(np.array([v for v, _ in cases]))
+    for (v, want), g in zip(cases, got):
+        assert g == want, (v, hex(g), hex(want))
+
+
+# --------------------------------------------------------------------------- quantisation
+
+
+def _exact_bf16_of(x: Fraction) -> int:
+    """bfloat16 bits of the exact rational x, rounded to nearest, ties to even (normal range only)."""
+    if x == 0:
+        return 0
+    s = 0x8000 if x < 0 else 0
+    a = abs(x)
+    e = math.floor(math.log2(a))
+    while Fraction(2) ** e > a:
+        e -= 1
+    while Fraction(2) ** (e + 1) <= a:
+        e += 1
+    ulp = Fraction(2) ** (e - 7)
+    m = a / ulp                      # in [128, 256)
+    fl = math.floor(m)
+    rem = m - fl
+    if rem > Fraction(1, 2) or (rem == Fraction(1, 2) and fl % 2 == 1):
+        fl += 1
+    val = float(fl * ulp)
+    return s | (int(np.array(val, np.float32).view(np.uint32)) >> 16)
+
+
+def test_quantise_matches_exact_normalisation():
+    """Normalise exactly (60-digit decimal sqrt, rational division) and round once: the oracle agrees."""
+    getcontext().prec = 60
+    rng = np.random.default_rng(7)
+    x = rng.standard_normal((40, 16)).astype(np.float32)
+    x[3] *= 1e-20
+    x[4] *= 1e20
+    got = oracle.quantise(x, oracle.F32)
+    for r in range(x.shape[0]):
+        ss = sum(Fraction(float(v)) ** 2 for v in x[r])
+        n = Fraction(Decimal(ss.numerator) / Decimal(ss.denominator)).limit_denominator(10 ** 55)
+        n = Fraction(Decimal(n.numerator / Decimal(n.denominator)).sqrt())
+        for j in range(x.shape[1]):
+            want = _exact_bf16_of(Fraction(float(x[r, j])) / n)
+            assert got[r, j] == want, (r, j)
+
+
+def test_quantise_closed_forms():
+    q = oracle.quantise(np.array([[3, 4, 0, 0], [0, 0, 7.5, 0], [1, 1, 1, 1], [0, 0, 0, 0],
+                                  [-2, 0, 0, 0]], np.float32), oracle.F32)
+    np.testing.assert_array_equal(q[0], [0x3F1A, 0x3F4D, 0, 0])     # 0.6 -> 0.6015625, 0.8 -> 0.80078125
+    np.testing.assert_array_equal(q[1], [0, 0, 0x3F80, 0])           # a basis vector normalises to 1.0
+    np.testing.assert_array_equal(q[2], [0x3F00] * 4)                # 1/2 each, exact
+    np.testing.assert_array_equal(q[3], [0, 0, 0, 0])                # zero stays zero
+    np.testing.assert_array_equal(q[4], [0xBF80, 0, 0, 0])
+
+
+def test_quantise_invariances_and_dtypes():
+    rng = np.random.default_rng(11)
+    x = rng.standard_normal((64, 96)).astype(np.float32)
+    q = oracle.quantise(x, oracle.F32)
+    # scaling by a power of two is exact and must not change the result
+    np.testing.assert_array_equal(oracle.quantise(x * np.float32(2.0 ** 37), oracle.F32), q)
+    np.testing.assert_array_equal(oracle.quantise(x * np.float32(2.0 ** -41), oracle.F32), q)
+    # negation flips exactly the sign bits
+    np.testing.assert_array_equal(oracle.quantise(-x, oracle.F32), q ^ np.uint16(0x8000))
+    # a bfloat16 input reads as the float it denotes
+    xb = torch_bf16(x)
+    np.testing.assert_array_equal(oracle.quantise(xb, oracle.BF16),
+                                  oracle.quantise(bf.widen(xb).astype(np.float32), oracle.F32))
+    # the quantised rows are unit vectors up to the bf16 rounding of each component
+    n = np.linalg.norm(bf.widen(q), axis=1)
+    assert np.all(np.abs(n - 1) <= U)
+
+
+# --------------------------------------------------------------------------- hand-derived lookup
+
+
+def test_handworked_example():
+    """A d=4 cache whose normalised vectors and scores are exact in bfloat16 and float.
+
+    keys   k0 = (1,1,1,1)      -> (1/2,1/2,1/2,1/2)
+           k1 = (1,1,1,-1)     -> (1/2,1/2,1/2,-1/2)
+           k2 = (2,0,0,0)      -> (1,0,0,0)
+           k3 = (3,3,3,3)      -> same as k0 (an exact duplicate after normalisation)
+           k4 = (0,0,0,0)      -> zero vector, scores 0 against everything
+    queries and their exact scores against k0..k4:
+      q0 = (1,1,1,1)           1, 1/2, 1/2, 1, 0      -> idx 0 (tie with 3: lowest), score 1
+      q1 = 5*(1,1,1,-1)        1/2, 1, 1/2, 1/2, 0    -> idx 1, score 1
+      q2 = (-1,0,0,0)          -1/2,-1/2,-1,-1/2, 0   -> idx 4 (the zero key wins with 0), score 0
+      q3 = (0,0,0,0)           0 everywhere            -> idx 0, score 0
+      q4 = (1,-1,1,-1)         0, 1/2, 1/2, 0, 0      -> idx 1 (tie with 2: lowest), score 1/2
+    tau_q = 1/2: q0, q1, q4 hit (q4 exactly at the threshold: ">="), q2, q3 miss.
+    stage 2 (tau_r = 1/2, k = 2):
+      q0 -> entry 0: tokens equal                              -> HIT_EXACT, r = e0.a0 = 1
+      q1 -> entry 1: tokens differ, r = e1.a1 = 1/2 (= tau_r)  -> HIT
+      q4 -> entry 1: tokens differ, r = e1.a4 = -1             -> REJECT
+    """
+    keys = np.array([[1, 1, 1, 1], [1, 1, 1, -1], [2, 0, 0, 0], [3, 3, 3, 3], [0, 0, 0, 0]], np.float32)
+    emb = np.array([[1, 0, 0, 0], [1, 1, 1, 1], [0, 1, 0, 0], [0, 0, 1, 0], [0, 0, 0, 1]], np.float32)
+    tokens = np.array([[5, 6, 7], [8, 9, 10], [1, 2, 3], [5, 6, 7], [0, 0, 0]], np.int32)
+    queries = np.array([[1, 1, 1, 1], [5, 5, 5, -5], [-1, 0, 0, 0], [0, 0, 0, 0], [1, -1, 1, -1]], np.float32)
+    la = np.array([[1, 0, 0, 0], [1, 1, 1, -1], [1, 0, 0, 0], [1, 0, 0, 0], [-1, -1, -1, -1]], np.float32)
+    la_tok = np.array([[5, 6], [8, 0], [1, 2], [0, 0], [8, 9 + 1]], np.int32)
+    c = oracle.OracleCache(4, 3, oracle.F32)
+    assert c.insert(keys, emb, tokens) == 0
+    out = c.lookup(queries, la, la_tok, 0.5, 0.5, 2)
+    np.testing.assert_array_equal(out["idx"], [0, 1, 4, 0, 1])
+    np.testing.assert_array_equal(out["score"], np.float32([1, 1, 0, 0, 0.5]))
+    np.testing.assert_array_equal(out["decision"], [HIT_EXACT, HIT, MISS, MISS, REJECT])
+    r = out["resp_score"]
+    assert r[0] == 1.0 and r[1] == 0.5 and r[4] == -1.0
+    assert np.isnan(r[2]) and np.isnan(r[3])
+    np.testing.assert_array_equal(out["margin"], [0.0, 0.5, 0.5, 0.0, 0.0])
+
+
+# --------------------------------------------------------------------------- brute force
+
+
+def _random_case(rng, N, d, B, k_cap, dup=0):
+    keys = oracle.quantise(rng.standard_normal((N, d)).astype(np.float32), oracle.F32)
+    if dup and N > 1:
+        src = rng.integers(0, N, dup)
+        dst = rng.integers(0, N, dup)
+        keys[dst] = keys[src]
+    emb = oracle.quantise(rng.standard_normal((N, d)).astype(np.float32), oracle.F32)
+    tokens = rng.integers(0, 50, (N, k_cap), dtype=np.int32)
+    q = oracle.quantise(rng.standard_normal((B, d)).astype(np.float32), oracle.F32)
+    a = oracle.quantise(rng.standard_normal((B, d)).astype(np.float32), oracle.F32)
+    return keys, emb, tokens, q, a
+
+
+@pytest.mark.parametrize("N,d,B,k_cap,k", [(1, 32, 5, 1, 1), (2, 32, 9, 8, 8), (7, 64, 16, 20, 20),
+                                           (300, 64, 33, 64, 64), (2000, 384, 64, 150, 150),
+                                           (1500, 96, 40, 150, 65)])
+def test_lookup_matches_bruteforce(N, d, B, k_cap, k):
+    rng = np.random.default_rng(N * 1000 + d)
+    keys, emb, tokens, q, a = _random_case(rng, N, d, B, k_cap, dup=N // 10)
+    # plant: some queries equal to stored keys (hits) with stored tokens (exact) or a near-far embedding
+    pick = rng.integers(0, N, B)
+    half = B // 2
+    q[:half] = keys[pick[:half]]
+    u = rng.integers(0, 50, (B, k), dtype=np.int32)
+    u[: half // 2] = tokens[pick[: half // 2], :k]
+    a[half // 2: half] = emb[pick[half // 2: half]]
+    for tau_q, tau_r in [(0.9, 0.85), (-1.0, -1.0), (0.0, 0.3), (1.5, 0.0)]:
+        o = oracle.lookup(keys, emb, tokens, q, a, u, tau_q, tau_r, k)
+        w = bf.lookup(keys, emb, tokens, q, a, u, tau_q, tau_r, k)
+        np.testing.assert_array_equal(o["idx"], w["idx"])
+        np.testing.assert_array_equal(o["score"], w["score"])
+        np.testing.assert_array_equal(o["decision"], w["decision"])
+        np.testing.assert_array_equal(o["resp_score"], w["resp_score"])  # NaN positions match too
+        S = w["S"]
+        best = S.max(axis=1)
+        second = np.where(S == best[:, None], -np.inf, S).max(axis=1)
+        n_best = (S == best[:, None]).sum(axis=1)
+        want_margin = np.where(n_best > 1, 0.0, best - second)
+        np.testing.assert_array_equal(o["margin"], want_margin)
+
+
+def test_decide_at_arbitrary_entry_matches_bruteforce():
+    rng = np.random.default_rng(5)
+    keys, emb, tokens, q, a = _random_case(rng, 50, 32, 20, 8)
+    u = rng.integers(0, 50, (20, 8), dtype=np.int32)
+    at = rng.integers(0, 50, 20).astype(np.int32)
+    q[:10] = keys[at[:10]]
+    u[:5] = tokens[at[:5]]
+    o = oracle.decide(keys, emb, tokens, q, a, u, 0.5, 0.1, 8, at)
+    S = bf.scores(q, keys)
+    np.testing.assert_array_equal(o["s"], S[np.arange(20), at])
+    for b in range(20):
+        one = bf.lookup(keys[at[b]:at[b] + 1], emb[at[b]:at[b] + 1], tokens[at[b]:at[b] + 1], q[b:b + 1],
+                        a[b:b + 1], u[b:b + 1], 0.5, 0.1, 8)
+        assert o["decision"][b] == one["decision"][0]
+        assert o["score"][b] == one["score"][0]
+
+
+def test_empty_and_single_entry():
+    rng = np.random.default_rng(3)
+    keys, emb, tokens, q, a = _random_case(rng, 1, 16, 4, 4)
+    u = rng.integers(0, 50, (4, 4), dtype=np.int32)
+    o = oracle.lookup(keys[:0], emb[:0], tokens[:0], q, a, u, 0.9, 0.85, 4)
+    np.testing.assert_array_equal(o["idx"], -1)
+    assert np.all(np.isnan(o["score"])) and np.all(np.isnan(o["resp_score"]))
+    np.testing.assert_array_equal(o["decision"], MISS)
+    o = oracle.lookup(keys, emb, tokens, q, a, u, -2.0, 0.85, 4)
+    np.testing.assert_array_equal(o["idx"], 0)
+    assert np.all(np.isinf(o["margin"]))
+
+
+# --------------------------------------------------------------------------- invariants
+
+
+def _store(rng, N, d, k_cap=8, vocab=1000):
+    keys = oracle.quantise(rng.standard_normal((N, d)).astype(np.float32), oracle.F32)
+    emb = oracle.quantise(rng.standard_normal((N, d)).astype(np.float32), oracle.F32)
+    tokens = rng.integers(0, vocab, (N, k_cap), dtype=np.int32)
+    return keys, emb, tokens
+
+
+def test_self_query_returns_itself_with_unit_score():
+    rng = np.random.default_rng(21)
+    raw = rng.standard_normal((3000, 64)).astype(np.float32)
+    c = oracle.OracleCache(64, 8, oracle.F32)
+    c.insert(raw, rng.standard_normal((3000, 64)).astype(np.float32), rng.integers(0, 9, (3000, 8)))
+    sel = rng.integers(0, 3000, 50)
+    out = c.lookup(raw[sel], raw[sel], c.tokens[sel], 0.9, 0.85, 8)
+    want = [oracle.first_identical(c.keys, i) for i in sel]
+    np.testing.assert_array_equal(out["idx"], want)
+    assert np.all(out["score"] <= 1.0) and np.all(out["score"] >= (1 - U) ** 2)
+    np.testing.assert_array_equal(out["decision"], HIT_EXACT)
+
+
+def test_scores_in_unit_interval_and_permutation_invariance():
+    rng = np.random.default_rng(22)
+    keys, emb, tokens = _store(rng, 2500, 48)
+    keys[100] = keys[7]                      # an exact duplicate pair
+    q = oracle.quantise(rng.standard_normal((40, 48)).astype(np.float32), oracle.F32)
+    q[0] = keys[100]
+    q[1] = keys[5]
+    a = q.copy()
+    u = rng.integers(0, 1000, (40, 8), dtype=np.int32)
+    o = oracle.lookup(keys, emb, tokens, q, a, u, 0.2, 0.1, 8)
+    assert np.all(np.abs(o["score"]) <= 1)
+    rs = o["resp_score"][~np.isnan(o["resp_score"])]
+    assert np.all(np.abs(rs) <= 1)
+    assert o["idx"][0] == 7
+    perm = rng.permutation(2500)
+    inv = np.argsort(perm)
+    p = oracle.lookup(keys[perm], emb[perm], tokens[perm], q, a, u, 0.2, 0.1, 8)
+    # the winner is the same entry, except that the duplicate pair now resolves to whichever copy comes first
+    same = inv[o["idx"]] == p["idx"]
+    dup_row = np.isin(o["idx"], [7, 100])
+    assert np.all(same | dup_row)
+    assert p["idx"][0] == min(inv[7], inv[100])
+    np.testing.assert_array_equal(p["score"], o["score"])
+    # stage 2 reads the winner's own prefix, which differs between the two copies of the duplicate
+    np.testing.assert_array_equal(p["decision"][~dup_row], o["decision"][~dup_row])
+    np.testing.assert_array_equal(p["resp_score"][~dup_row], o["resp_score"][~dup_row])
+    r0 = np.clip(np.float32(bf.widen(a[0]) @ bf.widen(emb[perm][p["idx"][0]])), -1, 1)
+    assert p["resp_score"][0] == r0
+
+
+def test_all_negative_scores():
+    rng = np.random.default_rng(23)
+    x = rng.standard_normal(32).astype(np.float32)
+    c = oracle.OracleCache(32, 2, oracle.F32)
+    c.insert(np.stack([x, 2 * x, x]), np.stack([x, x, x]), np.zeros((3, 2)))
+    out = c.lookup((-x)[None], x[None], np.zeros((1, 2)), -1.0, 0.0, 2)
+    assert out["idx"][0] == 0
+    assert -1.0 <= out["score"][0] <= -(1 - U) ** 2
+
+
+def test_planted_queries_closed_form_and_classes():
+    """q = c x + sqrt(1-c^2) v (v orthogonal to x) has cosine c with x: after the bf16 rounding of both
+    sides the oracle's score must stay within the rounding bound of c; benign plants are served
+    (HIT_EXACT), collisions rejected, misses missed -- the synthetic analogues of BHR = 1, AHR = 0."""
+    for name, N in [("tiny", 3000), ("mid", 3000)]:
+        w = synth.generate(name, N=N)
+        sp = w.spec
+        c = oracle.OracleCache(sp.d, sp.k_cap, sp.in_dtype)
+        c.insert(w.keys, w.emb, w.tokens)
+        o = c.lookup(w.queries, w.la_emb, w.la_tok, sp.tau_q, sp.tau_r, sp.k)
+        pl = w.cls != synth.CLS_MISS
+        # worst case: every component of both vectors moves by <= u relative, per rounding
+        bound = (2 * U + U * U) if sp.in_dtype == oracle.F32 else (4 * U + 6 * U * U)
+        err = np.abs(o["s_best"][pl] - w.cos[pl])
+        assert np.all(err <= bound), err.max()
+        assert err.mean() < 1e-3
+        np.testing.assert_array_equal(o["idx"][pl], w.target[pl])
+        clear = pl & (w.cos >= sp.tau_q + 2e-3)
+        ben = clear & (w.cls == synth.CLS_BENIGN)
+        col = clear & (w.cls == synth.CLS_COLLISION)
+        assert ben.sum() > 5 and col.sum() > 5
+        np.testing.assert_array_equal(o["decision"][ben], HIT_EXACT)
+        np.testing.assert_array_equal(o["decision"][col], REJECT)
+        np.testing.assert_array_equal(o["decision"][~pl], MISS)
+        below = pl & (w.cos < sp.tau_q - 2e-2)
+        np.testing.assert_array_equal(o["decision"][below], MISS)
+
+
+def test_threshold_special_cases():
+    rng = np.random.default_rng(24)
+    keys, emb, tokens = _store(rng, 500, 40)
+    q = oracle.quantise(rng.standard_normal((30, 40)).astype(np.float32), oracle.F32)
+    q[:10] = keys[:10]
+    a = oracle.quantise(rng.standard_normal((30, 40)).astype(np.float32), oracle.F32)
+    u = rng.integers(0, 1000, (30, 8), dtype=np.int32)
+    # tau_r <= -1: stage 2 always passes, leaving thresholded top-1 (MIPS) -- pinned by numpy's argmax
+    o = oracle.lookup(keys, emb, tokens, q, a, u, 0.1, -1.0, 8)
+    S = bf.scores(q, keys)
+    np.testing.assert_array_equal(o["idx"], np.argmax(S, axis=1))
+    hit = o["score"] >= np.float32(0.1)
+    assert np.all(np.isin(o["decision"][hit], [HIT, HIT_EXACT]))
+    np.testing.assert_array_equal(o["decision"][~hit], MISS)
+    # tau_q > 1: nothing is a hit, stage 2 never runs
+    o = oracle.lookup(keys, emb, tokens, q, a, u, 1.0001, 0.0, 8)
+    np.testing.assert_array_equal(o["decision"], MISS)
+    assert np.all(np.isnan(o["resp_score"]))
+
+
+def test_stage2_alone():
+    """Stage 2 is a dot product of the two quantised prefix embeddings and an equality of k tokens."""
+    rng = np.random.default_rng(25)
+    keys, emb, tokens = _store(rng, 1, 64, k_cap=16)
+    a = oracle.quantise(rng.standard_normal((6, 64)).astype(np.float32), oracle.F32)
+    a[0] = emb[0]
+    u = np.tile(tokens[0, :5], (6, 1))
+    u[2, 4] += 1                              # differs only in the last compared position
+    u[3, 0] += 1
+    q = np.tile(keys[0], (6, 1))
+    o = oracle.lookup(keys, emb, tokens, q, a, u, 0.5, 2.0, 5)   # tau_r > 1: only the token path can pass
+    r = np.clip(np.float32(bf.widen(a) @ bf.widen(emb[0])), -1, 1)
+    np.testing.assert_array_equal(o["resp_score"], r)
+    np.testing.assert_array_equal(o["decision"], [HIT_EXACT, HIT_EXACT, REJECT, REJECT, HIT_EXACT,
+                                                  HIT_EXACT])
+    # tokens equal but the embedding far: the identical-token rule decides (HIT_EXACT)
+    a2 = -emb[[0]]
+    o = oracle.lookup(keys, emb, tokens, keys[[0]], a2, tokens[[0], :5], 0.5, 0.9, 5)
+    assert o["decision"][0] == HIT_EXACT and o["resp_score"][0] < -0.99
+    # k = 1 compares only the first token; k = k_cap compares all of them
+    u1 = tokens[[0], :16].copy()
+    u1[0, 15] += 1
+    assert oracle.lookup(keys, emb, tokens, keys[[0]], -emb[[0]], u1[:, :1], 0.5, 0.9, 1)["decision"][0] == HIT_EXACT
+    assert oracle.lookup(keys, emb, tokens, keys[[0]], -emb[[0]], u1, 0.5, 0.9, 16)["decision"][0] == REJECT
+
+
+def test_paper_thresholds_fixture():
+    """The paper-shaped workload uses the thresholds and window the paper calibrates (Appendix A.2)."""
+    import json
+    import os
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "paper_thresholds.json")))
+    sp = synth.spec("mid_paper")
+    bge = g["tau_c"]["BGE"]
+    assert np.float32(sp.tau_q) == np.float32(min(bge["cap"], bge["P5"]))
+    qb = g["tau_a"]["Qwen3+BGE"]
+    assert np.float32(sp.tau_r) == np.float32(min(qb["cap"], qb["P10"]))
+    assert sp.k == g["k"] and sp.d == g["embedding_dim"]["BGE"]
+    for name, row in g["tau_a"].items():
+        assert abs(min(row["cap"], row["P10"]) - row["used"]) < 1e-9, name
