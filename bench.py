@@ -1,0 +1,199 @@
+"""Throughput of the two-stage LaCache lookup on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload serve_large|serve_small]
+
+A step is one lookup call through the C ABI -- query normalisation, stage 1
+(top-1 over all cached keys) and stage 2 (gather and verify of the hits) -- on
+a batch of synthetic queries against a cache of 1,000,000 entries, d = 768,
+bfloat16 inputs, k = 16, whose inputs already sit in device memory.
+
+The headline workload (`value`) is serve_large: 4096 queries per call (the
+matrix-core-bound regime); serve_small (16 queries per call, the HBM-bound
+regime) is measured in the same run and reported under "secondary".  For
+each, "roofline" rates the stage-1 kernel, timed with HIP events recorded by
+the library on the launch stream, against the MI355X peak (bf16 dense MFMA
+2.5 PFLOP/s, HBM 8 TB/s).  "cpu_baseline" times the CPU oracle on a bounded
+sample of the same workload on the host cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="serve_large", choices=["serve_large", "serve_small"])
+    ap.add_argument("--no-secondary", action="store_true", help="measure only the headline workload")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
+    ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
+                    help="per-launch HBM traffic measured with rocprofv3 counters (JSON), if present")
+    return ap.parse_args()
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def describe(sp, call_b):
+    return (f"{sp.name}: N={sp.N:,} cached entries, d={sp.d} bf16 keys and prefix embeddings, k={sp.k} prefix "
+            f"tokens, vocab {sp.vocab}, B={call_b} queries per call "
+            f"({sp.frac_benign:.0%} benign / {sp.frac_collision:.0%} collision / rest miss"
+            + (f", {sp.n_dup} exact-duplicate key pairs" if sp.n_dup else "") + ")")
+
+
+def run_workload(name, steps, warmup, lc, torch, synth, traffic_db, want_cpu):
+    from tests.gpu_util import gpu_cache, to_dev
+    sp = synth.spec(name)
+    call_b = synth.SERVE_SMALL_CALL_B if name == "serve_small" else sp.B
+    t0 = time.time()
+    w = synth.generate(sp)
+    log(f"[bench] {name}: generated in {time.time() - t0:.1f}s")
+    c = gpu_cache(lc, sp, w.keys, w.emb, w.tokens, max_batch=max(call_b, 16), insert_chunk=1 << 18)
+    q, a = to_dev(w.queries), to_dev(w.la_emb)
+    t = to_dev(np.ascontiguousarray(w.la_tok[:, :sp.k]))
+    n_calls = sp.B // call_b
+    batches = [(q[i * call_b:(i + 1) * call_b], a[i * call_b:(i + 1) * call_b], t[i * call_b:(i + 1) * call_b])
+               for i in range(n_calls)]
+    dev = torch.device("cuda", 0)
+    outs = [tuple(torch.empty(call_b, dtype=dt, device=dev)
+                  for dt in (torch.int32, torch.float32, torch.float32, torch.int32)) for _ in range(n_calls)]
+
+    def step(i):
+        bq, ba, bt = batches[i % n_calls]
+        c.lookup(bq, ba, bt, sp.tau_q, sp.tau_r, sp.k, out=outs[i % n_calls])
+
+    for i in range(warmup):
+        step(i)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(steps):
+        step(i)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    # a second pass of the same steps with the library's stage-1 events on
+    c.profile(True)
+    for i in range(steps):
+        step(i)
+    torch.cuda.synchronize()
+    k_ms, k_n = c.profile_read()
+    c.profile(False)
+    k_avg = k_ms / max(k_n, 1)
+
+    # decisions of every query of the pool (synthetic hit-rate analogues of the paper's BHR / AHR)
+    dec = np.concatenate([outs[i][3].cpu().numpy() for i in range(n_calls)])
+    ben, col = w.cls == synth.CLS_BENIGN, w.cls == synth.CLS_COLLISION
+    served = np.isin(dec, [2, 3])
+    rates = dict(benign_hit_rate=float(served[ben].mean()), attack_hit_rate=float(served[col].mean()),
+                 miss_rate_of_misses=float((dec[w.cls == synth.CLS_MISS] == 0).mean()))
+
+    flops = 2.0 * call_b * sp.N * sp.d
+    key_bytes = float(sp.N) * sp.d * 2
+    if call_b >= 1024:
+        roof = dict(bound="mfma", achieved=flops / (k_avg * 1e-3) / 1e12, peak=PEAK_BF16_TFLOPS, unit="TFLOP/s")
+    else:
+        roof = dict(bound="hbm", achieved=key_bytes / (k_avg * 1e-3) / 1e9, peak=PEAK_HBM_GBS, unit="GB/s")
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = traffic_db.get(name)
+    roof["kernel_avg_ms"] = k_avg
+    res = dict(workload=name, value=call_b / (ms * 1e-3), unit="lookups/s", ms_per_step=ms, B=call_b,
+               roofline=roof, rates=rates, config=dict(workload=describe(sp, call_b), N=sp.N, d=sp.d, B=call_b,
+                                                       k=sp.k, k_cap=sp.k_cap, tau_q=sp.tau_q, tau_r=sp.tau_r))
+    if want_cpu:
+        res["cpu_baseline"] = cpu_baseline(sp, w, call_b)
+    c.close()
+    del w, q, a, t, batches
+    torch.cuda.empty_cache()
+    return res
+
+
+def cpu_baseline(sp, w, call_b):
+    """The CPU oracle, as it is, on a bounded sample: a few queries against the full cache."""
+    import oracle
+    t0 = time.time()
+    kq = oracle.quantise(w.keys, sp.in_dtype)
+    eq = oracle.quantise(w.emb, sp.in_dtype)
+    t_store = time.time() - t0
+    threads = oracle.num_threads()
+    n = max(threads, 16)
+    qq = oracle.quantise(w.queries[:n], sp.in_dtype)
+    aq = oracle.quantise(w.la_emb[:n], sp.in_dtype)
+    u = np.ascontiguousarray(w.la_tok[:n, :sp.k])
+    t0 = time.perf_counter()
+    oracle.lookup(kq, eq, w.tokens, qq, aq, u, sp.tau_q, sp.tau_r, sp.k)
+    el = time.perf_counter() - t0
+    return dict(value=n / el, unit="lookups/s", cores=threads, kind="oracle",
+                sample=f"{n} queries of the same pool against all {sp.N:,} entries (queries quantised outside the "
+                       f"timed call; store quantisation {t_store:.1f}s not counted), {el:.1f}s")
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU only: the lookup is built and measured on a single MI355X; "
+              "sharding the cache over GPUs is a design note, not part of this build.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import synth
+    from paper_2608_01718_amd import build as b
+    if not os.path.exists(b.OUT):
+        b.build()
+    import paper_2608_01718_amd as lc
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    traffic_db = {}
+    if os.path.exists(args.traffic):
+        traffic_db = json.load(open(args.traffic))
+
+    main_res = run_workload(args.workload, args.steps, args.warmup, lc, torch, synth, traffic_db, not args.no_cpu)
+    secondary = None
+    if not args.no_secondary:
+        other = "serve_small" if args.workload == "serve_large" else "serve_large"
+        secondary = run_workload(other, args.steps, args.warmup, lc, torch, synth, traffic_db, False)
+
+    line = {
+        "metric": "cache lookups/sec (2-stage) at N=1M,d=768; % HBM / MFMA roofline",
+        "value": main_res["value"],
+        "unit": "lookups/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": main_res["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded Gaussian embeddings with planted benign / collision / miss queries)",
+        "config": main_res["config"],
+        "roofline": {k: main_res["roofline"][k] for k in ("bound", "achieved", "peak", "unit", "frac", "traffic")},
+        "stage1_kernel_avg_ms": main_res["roofline"]["kernel_avg_ms"],
+        "rates": main_res["rates"],
+        "cpu_baseline": main_res.get("cpu_baseline"),
+    }
+    if secondary:
+        line["secondary"] = {
+            "workload": secondary["config"]["workload"], "value": secondary["value"], "unit": "lookups/s",
+            "ms_per_step": secondary["ms_per_step"],
+            "roofline": {k: secondary["roofline"][k] for k in ("bound", "achieved", "peak", "unit", "frac",
+                                                                  "traffic")},
+            "stage1_kernel_avg_ms": secondary["roofline"]["kernel_avg_ms"], "rates": secondary["rates"]}
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

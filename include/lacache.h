@@ -1,0 +1,160 @@
+/*
+ * lacache.h -- C ABI of the LaCache two-stage semantic-cache lookup for
+ * AMD Instinct MI355X (gfx950).
+ *
+ * The method (LaCache, "Robust Semantic Caching for LLM Serving"):
+ *   - Each cache entry is <h(x), [h(f_k(x)), f(x)]> (Section 4.2, cache
+ *     structure): the key of the cached query x, a lookahead key of the first
+ *     k tokens of its response, and the response itself.  Here the key is the
+ *     L2-normalised query embedding, the lookahead key is the normalised
+ *     embedding of the response prefix plus the k prefix token IDs, and the
+ *     response f(x) stays with the caller, addressed by the entry index.
+ *   - A query is processed in two stages (Algorithm 1, Section 4.2 query
+ *     processing).  Stage 1 searches the cache with the query key: the entry
+ *     of highest cosine similarity is the candidate, a hit when its
+ *     similarity is >= tau_q (Section 5.1: cache check sim(x, x') >= tau_c).
+ *     Stage 2 runs only on a stage-1 hit: the lookahead of the new query
+ *     (its first k speculatively decoded tokens and their embedding) is
+ *     compared with the stored prefix of the matched entry; it passes when
+ *     the k tokens are identical or the prefix-embedding cosine is >= tau_r
+ *     (Section 5.1: lookahead check sim(f_k(x), f_k(x')) >= tau_a).  Only
+ *     when both pass is the cached response served; otherwise the caller
+ *     decodes and inserts (Algorithm 1, fallback branch).
+ *
+ * Conventions for every function below:
+ *   - Every array argument is a DEVICE pointer on the handle's device (for
+ *     example a PyTorch ROCm tensor's data_ptr()), row-major and contiguous,
+ *     unless marked "host".  Pointers may be NULL only when the matching
+ *     count is 0.
+ *   - `stream` is a hipStream_t (NULL = the default stream).  insert, lookup
+ *     and export only enqueue work on it and return without waiting; the
+ *     caller keeps every buffer alive until the stream has passed the call.
+ *     Work on one handle must be ordered on one stream (or by events): calls
+ *     share the handle's store and scratch buffers.
+ *   - A handle is not thread-safe.
+ *   - Errors are returned as negative codes and nothing is enqueued when an
+ *     argument check fails.  No C++ exception crosses this interface.
+ *   - Vector inputs must be finite; non-finite components give unspecified
+ *     (but memory-safe) results.
+ */
+#ifndef LACACHE_H
+#define LACACHE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct lacache_s *lacache_t;
+
+/* dtype of every input vector of a cache (keys, prefix embeddings, queries, lookahead embeddings) */
+typedef enum { LACACHE_F32 = 0, LACACHE_BF16 = 1 } lacache_dtype;
+
+/* decision[b] of a lookup */
+enum {
+    LACACHE_MISS = 0,      /* stage 1 found no entry with similarity >= tau_q; stage 2 did not run */
+    LACACHE_REJECT = 1,    /* stage-1 hit whose lookahead check failed: a collision, decode and insert */
+    LACACHE_HIT = 2,       /* both checks passed through the prefix-embedding similarity */
+    LACACHE_HIT_EXACT = 3  /* both checks passed with identical first-k prefix tokens */
+};
+
+/* return codes */
+enum {
+    LACACHE_OK = 0,
+    LACACHE_EINVAL = -1,   /* bad argument (null pointer, size out of range, non-finite threshold) */
+    LACACHE_EFULL = -2,    /* insert would exceed the capacity; nothing was inserted */
+    LACACHE_ENOMEM = -3,   /* device allocation failed */
+    LACACHE_EHIP = -4      /* a HIP runtime call or kernel launch failed */
+};
+
+/*
+ * Create a cache on `device` for up to `capacity` entries (1 <= capacity <
+ * 2^31 - 256) of dimension d (1 <= d <= 16384), each storing k_cap prefix
+ * tokens (1 <= k_cap <= 4096).  Every input vector has dtype in_dtype.
+ * max_batch (1 <= max_batch <= 65536) sizes the lookup scratch; lookups with
+ * more queries are processed in chunks of max_batch.  All device memory
+ * (store and scratch) is allocated here, once, and zero-filled: the store
+ * takes capacity * (2 * d_pad * 2 + 4 * k_cap) bytes with d_pad = d rounded
+ * up to a multiple of 128.  On success *out receives the handle.
+ */
+int lacache_create(lacache_t *out, int64_t capacity, int32_t d, int32_t k_cap, lacache_dtype in_dtype,
+                   int32_t max_batch, int32_t device);
+
+/* Wait for the device, free everything the handle owns, and the handle itself. NULL is a no-op. */
+int lacache_destroy(lacache_t h);
+
+/*
+ * Append n entries (Algorithm 1: after decoding, the new entry is added to
+ * the cache).  keys and resp_emb are [n][d] of the cache's dtype (the query
+ * key and the embedding of the first k_cap response tokens, both from the
+ * same embedding model); resp_tokens is [n][k_cap] int32.  Keys and
+ * embeddings are L2-normalised (in double) and rounded once, to nearest-even,
+ * to bfloat16 as they are stored; a zero vector is stored as zero.
+ * Entries get indices size .. size+n-1 in order; *first_idx (host) receives
+ * the first.  The entry count is updated immediately, so later lookups on
+ * the same stream see the new entries.  n == 0 is a no-op.  Returns
+ * LACACHE_EFULL, inserting nothing, if n > capacity - size.
+ */
+int lacache_insert(lacache_t h, const void *keys, const void *resp_emb, const int32_t *resp_tokens, int32_t n,
+                   int64_t *first_idx, void *stream);
+
+/*
+ * Two-stage lookup of B queries (Algorithm 1).
+ *   queries          [B][d]  query embeddings (cache dtype)
+ *   lookahead_emb    [B][d]  embedding of each query's first k decoded tokens (cache dtype)
+ *   lookahead_tokens [B][k]  int32 token IDs of that prefix
+ *   tau_q, tau_r     finite thresholds of stage 1 and stage 2 (compared with >=)
+ *   k                1 <= k <= k_cap: number of prefix tokens compared
+ * Outputs, each [B]:
+ *   idx         entry of highest cosine similarity (lowest index among exact
+ *               ties), reported even on a miss; -1 only when the cache is empty
+ *   score       that similarity, clamped to [-1, 1]; NaN when the cache is empty
+ *   resp_score  prefix-embedding cosine with entry idx, clamped to [-1, 1];
+ *               quiet NaN (0x7FC00000) when stage 2 did not run
+ *   decision    LACACHE_MISS / REJECT / HIT / HIT_EXACT
+ * Similarities are dot products of the bfloat16-rounded normalised vectors,
+ * accumulated in float32.  B == 0 is a no-op.
+ */
+int lacache_lookup(lacache_t h, const void *queries, const void *lookahead_emb, const int32_t *lookahead_tokens,
+                   int32_t B, float tau_q, float tau_r, int32_t k, int32_t *idx, float *score, float *resp_score,
+                   int32_t *decision, void *stream);
+
+/* Number of entries inserted so far (host-side count); -1 for a NULL handle. */
+int64_t lacache_size(lacache_t h);
+
+/*
+ * Copy entries first .. first+n-1 of the store out, as stored: keys_bf16 and
+ * emb_bf16 are [n][d] bfloat16 bit patterns, tokens [n][k_cap] int32.  Any of
+ * the three may be NULL to skip it.  Requires 0 <= first, n >= 0,
+ * first + n <= size.  For inspection and tests.
+ */
+int lacache_export(lacache_t h, int64_t first, int32_t n, uint16_t *keys_bf16, uint16_t *emb_bf16, int32_t *tokens,
+                   void *stream);
+
+/*
+ * Batch-size crossover of stage 1: batches of at most b_small queries use the
+ * bandwidth-bound streaming kernel, larger ones the matrix-core GEMM kernel.
+ * 0 <= b_small <= 64 (default 64; 0 sends every batch to the GEMM kernel).
+ * Both kernels give the same results up to float32 summation order.
+ */
+int lacache_set_small_batch(lacache_t h, int32_t b_small);
+
+/*
+ * Timing of the stage-1 kernel.  While enabled, every lookup records a HIP
+ * event pair on its stream around its stage-1 launches.  profile_read waits
+ * for those events, returns the total elapsed milliseconds and the number of
+ * lookups timed (host pointers), and clears the record.  Enabling or
+ * disabling also clears it.
+ */
+int lacache_profile(lacache_t h, int32_t enable);
+int lacache_profile_read(lacache_t h, double *stage1_ms, int64_t *lookups);
+
+/* Static text for a return code. */
+const char *lacache_strerror(int code);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LACACHE_H */

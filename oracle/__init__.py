@@ -58,6 +58,7 @@ def lib():
         L.lco_decide.argtypes = [P, P, P, i64, i32, i32, P, P, P, i32, f32, f32, i32, P, P, P, P, P]
         L.lco_first_identical.argtypes = [P, i64, i32, i64]
         L.lco_first_identical.restype = i64
+        L.lco_num_threads.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -143,6 +144,11 @@ def decide(keys_q, emb_q, tokens, q_q, a_q, u, tau_q: float, tau_r: float, k: in
                      tau_q, tau_r, k, _ptr(at), _ptr(out["s"]), _ptr(out["score"]), _ptr(out["resp_score"]),
                      _ptr(out["decision"]))
     return out
+
+
+def num_threads() -> int:
+    """Threads the oracle's parallel loops use."""
+    return int(lib().lco_num_threads())
 
 
 def first_identical(keys_q, i: int) -> int:

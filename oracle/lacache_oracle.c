@@ -30,6 +30,7 @@
  * Decision codes: 0 MISS, 1 REJECT (collision detected), 2 HIT, 3 HIT_EXACT.
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <string.h>
 
@@ -255,4 +256,16 @@ void lco_bf16_rne_array(const double *in, int64_t n, uint16_t *out)
 {
     for (int64_t i = 0; i < n; ++i)
         out[i] = lco_bf16_rne(in[i]);
+}
+
+/* Threads an OpenMP parallel region of the oracle uses (reported beside its timings). */
+int lco_num_threads(void)
+{
+    int n = 1;
+#pragma omp parallel
+    {
+#pragma omp single
+        n = omp_get_num_threads();
+    }
+    return n;
 }

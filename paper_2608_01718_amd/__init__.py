@@ -1,0 +1,208 @@
+"""Python binding of liblacache (the gfx950 LaCache two-stage lookup): argument marshalling only.
+
+Every function mirrors one entry point of ``include/lacache.h`` under the
+same name and passes torch device tensors' data pointers and the current HIP
+stream straight through; all work runs in the library's kernels.  There is no
+fallback: importing this module fails if ``liblacache.so`` has not been built
+(``python -m paper_2608_01718_amd.build``).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "liblacache.so")
+
+MISS, REJECT, HIT, HIT_EXACT = 0, 1, 2, 3
+OK, EINVAL, EFULL, ENOMEM, EHIP = 0, -1, -2, -3, -4
+F32, BF16 = 0, 1
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2608_01718_amd.build` "
+                      "(there is no non-HIP implementation of the lookup)")
+
+_lib = ctypes.CDLL(LIB_PATH)
+_P, _i32, _i64, _f32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float
+_lib.lacache_create.argtypes = [ctypes.POINTER(_P), _i64, _i32, _i32, ctypes.c_int, _i32, _i32]
+_lib.lacache_destroy.argtypes = [_P]
+_lib.lacache_insert.argtypes = [_P, _P, _P, _P, _i32, ctypes.POINTER(_i64), _P]
+_lib.lacache_lookup.argtypes = [_P, _P, _P, _P, _i32, _f32, _f32, _i32, _P, _P, _P, _P, _P]
+_lib.lacache_size.argtypes = [_P]
+_lib.lacache_size.restype = _i64
+_lib.lacache_export.argtypes = [_P, _i64, _i32, _P, _P, _P, _P]
+_lib.lacache_set_small_batch.argtypes = [_P, _i32]
+_lib.lacache_profile.argtypes = [_P, _i32]
+_lib.lacache_profile_read.argtypes = [_P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_i64)]
+_lib.lacache_strerror.argtypes = [ctypes.c_int]
+_lib.lacache_strerror.restype = ctypes.c_char_p
+
+EXPORTED = ("lacache_create", "lacache_destroy", "lacache_insert", "lacache_lookup", "lacache_size",
+            "lacache_export", "lacache_set_small_batch", "lacache_profile", "lacache_profile_read",
+            "lacache_strerror")
+
+
+class LaCacheError(RuntimeError):
+    def __init__(self, code: int, what: str):
+        super().__init__(f"{what}: {lacache_strerror(code)} ({code})")
+        self.code = code
+
+
+def lacache_strerror(code: int) -> str:
+    return _lib.lacache_strerror(code).decode()
+
+
+def _check(code: int, what: str) -> None:
+    if code != OK:
+        raise LaCacheError(code, what)
+
+
+def _stream(device: int, stream) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream(device)
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _vec(t: torch.Tensor, dtype: int, rows: int, d: int, device: int, name: str) -> int:
+    want = (torch.float32,) if dtype == F32 else (torch.bfloat16, torch.int16, torch.uint16)
+    if t.dtype not in want or t.device.type != "cuda" or t.device.index != device:
+        raise ValueError(f"{name}: expected a {want} tensor on cuda:{device}, got {t.dtype} on {t.device}")
+    if tuple(t.shape) != (rows, d) or not t.is_contiguous():
+        raise ValueError(f"{name}: expected a contiguous [{rows}, {d}] tensor, got {tuple(t.shape)}")
+    return t.data_ptr()
+
+
+def _ints(t: torch.Tensor, shape, device: int, name: str) -> int:
+    if t.dtype != torch.int32 or t.device.type != "cuda" or t.device.index != device:
+        raise ValueError(f"{name}: expected an int32 tensor on cuda:{device}")
+    if tuple(t.shape) != tuple(shape) or not t.is_contiguous():
+        raise ValueError(f"{name}: expected a contiguous {list(shape)} tensor, got {tuple(t.shape)}")
+    return t.data_ptr()
+
+
+class LaCache:
+    """A handle of the C library plus the sizes it was created with."""
+
+    def __init__(self, capacity: int, d: int, k_cap: int, in_dtype: int = BF16, max_batch: int = 4096,
+                 device: int = 0):
+        self.capacity, self.d, self.k_cap, self.in_dtype = capacity, d, k_cap, in_dtype
+        self.max_batch, self.device = max_batch, device
+        h = _P()
+        _check(_lib.lacache_create(ctypes.byref(h), capacity, d, k_cap, in_dtype, max_batch, device),
+               "lacache_create")
+        self._h = h
+
+    @property
+    def handle(self):
+        if self._h is None:
+            raise ValueError("the cache has been destroyed")
+        return self._h
+
+    def insert(self, keys, resp_emb, resp_tokens, stream=None) -> int:
+        return lacache_insert(self, keys, resp_emb, resp_tokens, stream)
+
+    def lookup(self, queries, lookahead_emb, lookahead_tokens, tau_q, tau_r, k, out=None, stream=None):
+        return lacache_lookup(self, queries, lookahead_emb, lookahead_tokens, tau_q, tau_r, k, out, stream)
+
+    def export(self, first: int, n: int, stream=None):
+        return lacache_export(self, first, n, stream)
+
+    def size(self) -> int:
+        return lacache_size(self)
+
+    def set_small_batch(self, b_small: int) -> None:
+        lacache_set_small_batch(self, b_small)
+
+    def profile(self, enable: bool) -> None:
+        lacache_profile(self, enable)
+
+    def profile_read(self):
+        return lacache_profile_read(self)
+
+    def close(self) -> None:
+        if getattr(self, "_h", None) is not None:
+            lacache_destroy(self)
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def lacache_create(capacity: int, d: int, k_cap: int, in_dtype: int = BF16, max_batch: int = 4096,
+                   device: int = 0) -> LaCache:
+    return LaCache(capacity, d, k_cap, in_dtype, max_batch, device)
+
+
+def lacache_destroy(c: LaCache) -> None:
+    h, c._h = c._h, None
+    _check(_lib.lacache_destroy(h), "lacache_destroy")
+
+
+def lacache_insert(c: LaCache, keys, resp_emb, resp_tokens, stream=None) -> int:
+    n = keys.shape[0]
+    first = _i64(-1)
+    _check(_lib.lacache_insert(c.handle, _vec(keys, c.in_dtype, n, c.d, c.device, "keys"),
+                               _vec(resp_emb, c.in_dtype, n, c.d, c.device, "resp_emb"),
+                               _ints(resp_tokens, (n, c.k_cap), c.device, "resp_tokens"), n, ctypes.byref(first),
+                               _stream(c.device, stream)), "lacache_insert")
+    return first.value
+
+
+def lacache_lookup(c: LaCache, queries, lookahead_emb, lookahead_tokens, tau_q: float, tau_r: float, k: int,
+                   out=None, stream=None):
+    """Returns (idx int32, score f32, resp_score f32, decision int32), each [B], on the cache's device."""
+    B = queries.shape[0]
+    dev = torch.device("cuda", c.device)
+    if out is None:
+        out = (torch.empty(B, dtype=torch.int32, device=dev), torch.empty(B, dtype=torch.float32, device=dev),
+               torch.empty(B, dtype=torch.float32, device=dev), torch.empty(B, dtype=torch.int32, device=dev))
+    idx, score, resp, dec = out
+    for t, dt, nm in ((idx, torch.int32, "idx"), (score, torch.float32, "score"), (resp, torch.float32, "resp"),
+                      (dec, torch.int32, "decision")):
+        if t.dtype != dt or t.device != dev or t.numel() != B or not t.is_contiguous():
+            raise ValueError(f"{nm}: expected a contiguous [{B}] {dt} tensor on {dev}")
+    _check(_lib.lacache_lookup(c.handle, _vec(queries, c.in_dtype, B, c.d, c.device, "queries"),
+                               _vec(lookahead_emb, c.in_dtype, B, c.d, c.device, "lookahead_emb"),
+                               _ints(lookahead_tokens, (B, k), c.device, "lookahead_tokens"), B, float(tau_q),
+                               float(tau_r), int(k), idx.data_ptr(), score.data_ptr(), resp.data_ptr(),
+                               dec.data_ptr(), _stream(c.device, stream)), "lacache_lookup")
+    return out
+
+
+def lacache_size(c: LaCache) -> int:
+    return int(_lib.lacache_size(c.handle))
+
+
+def lacache_export(c: LaCache, first: int, n: int, stream=None):
+    """Returns (keys bf16-bits int16 [n][d], emb int16 [n][d], tokens int32 [n][k_cap]) as stored."""
+    dev = torch.device("cuda", c.device)
+    keys = torch.empty((n, c.d), dtype=torch.int16, device=dev)
+    emb = torch.empty((n, c.d), dtype=torch.int16, device=dev)
+    tok = torch.empty((n, c.k_cap), dtype=torch.int32, device=dev)
+    _check(_lib.lacache_export(c.handle, first, n, keys.data_ptr(), emb.data_ptr(), tok.data_ptr(),
+                               _stream(c.device, stream)), "lacache_export")
+    return keys, emb, tok
+
+
+def lacache_set_small_batch(c: LaCache, b_small: int) -> None:
+    _check(_lib.lacache_set_small_batch(c.handle, b_small), "lacache_set_small_batch")
+
+
+def lacache_profile(c: LaCache, enable: bool) -> None:
+    _check(_lib.lacache_profile(c.handle, 1 if enable else 0), "lacache_profile")
+
+
+def lacache_profile_read(c: LaCache):
+    """(total stage-1 milliseconds, number of lookups timed) since profiling was enabled or last read."""
+    ms, n = ctypes.c_double(0), _i64(0)
+    _check(_lib.lacache_profile_read(c.handle, ctypes.byref(ms), ctypes.byref(n)), "lacache_profile_read")
+    return ms.value, n.value
+
+
+def raw_library() -> ctypes.CDLL:
+    """The loaded C library, for callers that pass raw pointers themselves."""
+    return _lib

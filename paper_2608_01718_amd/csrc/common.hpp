@@ -1,0 +1,112 @@
+// common.hpp -- types, store layout and device helpers shared by the gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace lacache {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+constexpr int kWave = 64;
+
+// ---------------------------------------------------------------------------
+// Store layout of the normalised bfloat16 keys ("tiled"):
+//   a 16-row x 32-column block of the key matrix is one contiguous 1 KiB
+//   "chunk", ordered [c = col/8 % 4][r = row % 16][e = col % 8];
+//   chunks are ordered [row/16][col/32].
+// Lane l of a wave reading the chunk as 64 x 16 bytes gets row l%16 and
+// columns 8*(l/16) .. 8*(l/16)+7 -- exactly the A/B operand fragment of
+// v_mfma_f32_16x16x32_bf16 -- so every operand load is one fully coalesced
+// 1 KiB wave access, and a run of 16 keys is d_pad*32 contiguous bytes.
+// The same layout holds the normalised queries in scratch.
+// ---------------------------------------------------------------------------
+__host__ __device__ inline int64_t tiled_offset(int64_t row, int32_t col, int32_t kc /* d_pad / 32 */) {
+    return ((row >> 4) * kc + (col >> 5)) * 512 + (((col >> 3) & 3) * 16 + (row & 15)) * 8 + (col & 7);
+}
+
+// ---------------------------------------------------------------------------
+// Rounding of a double to bfloat16, once, to nearest with ties to even.
+// Normal range (|v| >= 2^-126): round the 52-bit double significand to 7
+// stored bits by adding just under half an ulp plus the kept lsb and
+// truncating; a carry moves into the exponent by itself.  Below 2^-126 the
+// bfloat16 grid is uniform with spacing 2^-133 (subnormals): round v*2^133 to
+// an integer.  Overflow gives infinity.
+// ---------------------------------------------------------------------------
+__device__ inline uint16_t bf16_rne_from_f64(double v) {
+    const uint64_t b = (uint64_t)__double_as_longlong(v);
+    const uint16_t sign = (uint16_t)((b >> 48) & 0x8000u);
+    const uint64_t mag = b & 0x7FFFFFFFFFFFFFFFull;
+    const int e = (int)(mag >> 52) - 1023;
+    if (e >= -126) {
+        uint64_t m = mag + ((1ull << 44) - 1) + ((mag >> 45) & 1);
+        const int e2 = (int)(m >> 52) - 1023;
+        if (e2 > 127) return (uint16_t)(sign | 0x7F80u);
+        return (uint16_t)(sign | ((uint32_t)(e2 + 127) << 7) | (uint32_t)((m >> 45) & 0x7F));
+    }
+    const double s = __builtin_rint(__builtin_ldexp(__builtin_fabs(v), 133));
+    return (uint16_t)(sign | (uint16_t)s);
+}
+
+__device__ inline float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+
+// Element j of a row of input vectors as a double (dtype 0 = float32, 1 = bfloat16).
+__device__ inline double load_in(const void* row, int dtype, int j) {
+    if (dtype == 0) return (double)((const float*)row)[j];
+    return (double)bf16_to_f32(((const uint16_t*)row)[j]);
+}
+
+// ---------------------------------------------------------------------------
+// Wave-wide butterfly reductions: every lane ends with the same value, and
+// the combination order is fixed, so results are run-to-run identical.
+// ---------------------------------------------------------------------------
+__device__ inline double wave_sum_f64(double x) {
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) x += __shfl_xor(x, m, kWave);
+    return x;
+}
+__device__ inline float wave_sum_f32(float x) {
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) x += __shfl_xor(x, m, kWave);
+    return x;
+}
+__device__ inline uint64_t umax64(uint64_t a, uint64_t b) { return a > b ? a : b; }
+__device__ inline uint64_t wave_max_u64(uint64_t x) {
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) x = umax64(x, (uint64_t)__shfl_xor((unsigned long long)x, m, kWave));
+    return x;
+}
+
+// ---------------------------------------------------------------------------
+// Top-1 candidates as one 64-bit key: high word = the score's bits mapped so
+// that unsigned order equals float order, low word = ~index.  The unsigned
+// maximum is then "highest score, lowest index among equal scores": a total
+// order, so any merge order gives the same winner.  -0 is folded onto +0
+// first so that equal scores compare equal.
+// ---------------------------------------------------------------------------
+__device__ inline uint32_t order_f32(float f) {
+    const uint32_t u = __float_as_uint(f + 0.0f);
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ inline float unorder_f32(uint32_t o) {
+    return __uint_as_float((o & 0x80000000u) ? (o & 0x7FFFFFFFu) : ~o);
+}
+__device__ inline uint64_t pack_top1(float s, int32_t idx) {
+    return ((uint64_t)order_f32(s) << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)idx);
+}
+__device__ inline int32_t unpack_idx(uint64_t p) { return (int32_t)(0xFFFFFFFFu - (uint32_t)(p & 0xFFFFFFFFu)); }
+__device__ inline float unpack_score(uint64_t p) { return unorder_f32((uint32_t)(p >> 32)); }
+
+__device__ inline f32x4 mfma16x16x32(u32x4 a, u32x4 b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c,
+                                                   0, 0, 0);
+}
+__device__ inline f32x16 mfma32x32x16(u32x4 a, u32x4 b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c,
+                                                   0, 0, 0);
+}
+
+}  // namespace lacache

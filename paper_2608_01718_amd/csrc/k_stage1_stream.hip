@@ -1,0 +1,152 @@
+// k_stage1_stream.hip -- stage 1 for small batches (B <= 64): one pass over the keys at HBM speed.
+//
+// Stage 1 of the lookup (Algorithm 1: search the cache with the query key) is
+// an exact top-1 over every stored key by the dot product of normalised
+// vectors.  With B <= 64 queries a key byte feeds at most 64 multiply-adds,
+// far below the matrix-core/HBM balance point, so the kernel is bound by
+// reading the keys once: every wave streams a contiguous run of 16-key groups
+// (d_pad*32 contiguous bytes each) with 1 KiB coalesced loads, double
+// buffered, while the queries sit in LDS for the whole launch.  Dot products
+// run on v_mfma_f32_16x16x32_bf16 with the keys as the row operand, so each
+// lane accumulates 4 keys x 1 query and keeps a running (best score, index)
+// per query in registers; rows are visited in increasing order and only a
+// strictly larger score replaces the best, so the lowest index wins ties.
+#include "common.hpp"
+#include "launch.hpp"
+
+namespace lacache {
+
+constexpr int kStreamWaves = 16;  // waves per workgroup; one workgroup per CU
+
+template <int QG>
+__global__ __launch_bounds__(1024) void k_stage1_stream(const u32x4* __restrict__ keys, const u32x4* __restrict__ qt,
+                                                        int kc, int groups, int n_rows, int waves_total, int B,
+                                                        uint64_t* __restrict__ part) {
+    extern __shared__ u32x4 smem[];
+    u32x4* qs = smem;                                        // [QG][kc][64] query fragments
+    uint64_t* red = (uint64_t*)(smem + QG * kc * 64);        // [kStreamWaves][QG * 16]
+    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+    for (int i = tid; i < QG * kc * 64; i += kStreamWaves * 64) qs[i] = qt[i];
+    __syncthreads();
+
+    float best[QG];
+    int bidx[QG];
+#pragma unroll
+    for (int q = 0; q < QG; ++q) {
+        best[q] = -__builtin_inff();
+        bidx[q] = 0x7FFFFFFF;
+    }
+
+    // contiguous, balanced split of the 16-key groups over all waves of the grid
+    const int64_t w = (int64_t)blockIdx.x * kStreamWaves + wid;
+    const int g0 = (int)(w * groups / waves_total);
+    const int g1 = (int)((w + 1) * groups / waves_total);
+    const int nchunks = (g1 - g0) * kc;
+    const u32x4* kp = keys + (int64_t)g0 * kc * 64 + lane;
+
+    u32x4 cur[4], nxt[4];
+    if (nchunks > 0) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) cur[u] = kp[u * 64];
+    }
+    f32x4 acc[QG];
+#pragma unroll
+    for (int q = 0; q < QG; ++q) acc[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+    int ks = 0, g = g0;
+    for (int c = 0; c < nchunks; c += 4) {
+        if (c + 4 < nchunks) {
+#pragma unroll
+            for (int u = 0; u < 4; ++u) nxt[u] = kp[(int64_t)(c + 4 + u) * 64];
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+#pragma unroll
+            for (int q = 0; q < QG; ++q) acc[q] = mfma16x16x32(cur[u], qs[(q * kc + ks + u) * 64 + lane], acc[q]);
+        }
+        ks += 4;
+        if (ks == kc) {
+            // lane holds rows 4*(lane/16)+j of the group, query column lane%16
+            const int row0 = g * 16 + 4 * (lane >> 4);
+#pragma unroll
+            for (int q = 0; q < QG; ++q) {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const float s = acc[q][j];
+                    if (row0 + j < n_rows && s > best[q]) {
+                        best[q] = s;
+                        bidx[q] = row0 + j;
+                    }
+                }
+                acc[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+            }
+            ks = 0;
+            ++g;
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) cur[u] = nxt[u];
+    }
+
+    // lanes l, l^16, l^32, l^48 hold the same query: merge, then merge the waves
+#pragma unroll
+    for (int q = 0; q < QG; ++q) {
+        uint64_t p = (bidx[q] == 0x7FFFFFFF) ? 0ull : pack_top1(best[q], bidx[q]);
+        p = umax64(p, (uint64_t)__shfl_xor((unsigned long long)p, 16, kWave));
+        p = umax64(p, (uint64_t)__shfl_xor((unsigned long long)p, 32, kWave));
+        if (lane < 16) red[wid * (QG * 16) + q * 16 + lane] = p;
+    }
+    __syncthreads();
+    if (tid < QG * 16 && tid < B) {
+        uint64_t m = 0;
+        for (int v = 0; v < kStreamWaves; ++v) m = umax64(m, red[v * (QG * 16) + tid]);
+        part[(int64_t)tid * gridDim.x + blockIdx.x] = m;
+    }
+}
+
+template <int QG>
+static hipError_t launch_qg(const u32x4* keys, const u32x4* qt, int kc, int groups, int n_rows, int nwg, int B,
+                            uint64_t* part, hipStream_t s) {
+    const size_t lds = (size_t)QG * kc * 1024 + (size_t)kStreamWaves * QG * 16 * 8;
+    static bool attr_set = false;
+    if (!attr_set) {
+        hipError_t e = hipFuncSetAttribute((const void*)k_stage1_stream<QG>,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+        if (e != hipSuccess) return e;
+        attr_set = true;
+    }
+    k_stage1_stream<QG><<<dim3(nwg), dim3(kStreamWaves * 64), lds, s>>>(keys, qt, kc, groups, n_rows,
+                                                                         nwg * kStreamWaves, B, part);
+    return hipGetLastError();
+}
+
+// Largest query-group count QG (16 queries each, at most 4) whose query
+// fragments fit in LDS next to the reduction area, for d_pad columns.
+int stream_max_qg(int d_pad) {
+    const int kc = d_pad / 32;
+    for (int qg = 4; qg >= 1; --qg)
+        if ((size_t)qg * kc * 1024 + (size_t)kStreamWaves * qg * 16 * 8 <= 160 * 1024) return qg;
+    return 0;
+}
+
+hipError_t launch_stage1_stream(const uint16_t* keys, const uint16_t* qt, int B, int n_rows, int d_pad,
+                                uint64_t* part, int num_cu, int* P_out, hipStream_t s) {
+    const int kc = d_pad / 32;
+    const int groups = (n_rows + 15) / 16;
+    const int qg = (B + 15) / 16;
+    if (qg < 1 || qg > stream_max_qg(d_pad) || kc % 4 != 0 || n_rows <= 0) return hipErrorInvalidValue;
+    // one workgroup per CU, fewer when there is too little work to give every wave >= 4 groups
+    int nwg = (groups + kStreamWaves * 4 - 1) / (kStreamWaves * 4);
+    if (nwg > num_cu) nwg = num_cu;
+    if (nwg > kMaxPartials) nwg = kMaxPartials;
+    if (nwg < 1) nwg = 1;
+    *P_out = nwg;
+    const u32x4* k4 = (const u32x4*)keys;
+    const u32x4* q4 = (const u32x4*)qt;
+    switch (qg) {
+        case 1: return launch_qg<1>(k4, q4, kc, groups, n_rows, nwg, B, part, s);
+        case 2: return launch_qg<2>(k4, q4, kc, groups, n_rows, nwg, B, part, s);
+        case 3: return launch_qg<3>(k4, q4, kc, groups, n_rows, nwg, B, part, s);
+        default: return launch_qg<4>(k4, q4, kc, groups, n_rows, nwg, B, part, s);
+    }
+}
+
+}  // namespace lacache

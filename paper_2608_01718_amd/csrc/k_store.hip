@@ -1,0 +1,95 @@
+// k_store.hip -- normalise-and-store kernels (insert, query staging) and the store export.
+//
+// Cosine similarity (Section 3: the distance of embeddings is e.g. the cosine
+// distance; Section 5.1: hits are decided on cosine similarities) is computed
+// as the dot product of L2-normalised vectors.  Each vector is normalised in
+// double and rounded once, to nearest-even, to bfloat16 as it is written, so a
+// query equal to a stored key quantises bit-identically to it.
+#include "common.hpp"
+#include "launch.hpp"
+
+namespace lacache {
+
+// One wave per row.  Rows >= rows (up to rows_pad) are written as zeros, as
+// are the columns d .. d_pad-1.  Lane l owns columns 8l + 512t .. 8l + 512t + 7.
+template <bool TILED>
+__global__ __launch_bounds__(256) void k_normalise_rows(const void* __restrict__ in, int dtype, int64_t rows,
+                                                        int64_t rows_pad, int d, int d_pad,
+                                                        uint16_t* __restrict__ out, int64_t row0) {
+    const int lane = threadIdx.x & 63;
+    const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (r >= rows_pad) return;
+    const bool live = r < rows;
+    const char* src = (const char*)in + (live ? r * (int64_t)d * (dtype == 0 ? 4 : 2) : 0);
+
+    double ss = 0.0;
+    if (live) {
+        for (int j0 = lane * 8; j0 < d; j0 += 512) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int j = j0 + e;
+                if (j < d) {
+                    const double v = load_in(src, dtype, j);
+                    ss += v * v;
+                }
+            }
+        }
+    }
+    ss = wave_sum_f64(ss);
+    const double n = __builtin_sqrt(ss);
+    const int kc = d_pad >> 5;
+    for (int j0 = lane * 8; j0 < d_pad; j0 += 512) {
+        uint16_t h[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const int j = j0 + e;
+            h[e] = 0;
+            if (live && j < d && n != 0.0) h[e] = bf16_rne_from_f64(load_in(src, dtype, j) / n);
+        }
+        u32x4 w;
+        w.x = (uint32_t)h[0] | ((uint32_t)h[1] << 16);
+        w.y = (uint32_t)h[2] | ((uint32_t)h[3] << 16);
+        w.z = (uint32_t)h[4] | ((uint32_t)h[5] << 16);
+        w.w = (uint32_t)h[6] | ((uint32_t)h[7] << 16);
+        const int64_t off = TILED ? tiled_offset(row0 + r, j0, kc) : (row0 + r) * (int64_t)d_pad + j0;
+        *(u32x4*)(out + off) = w;
+    }
+}
+
+// Copy rows first .. first+n-1 of a bfloat16 matrix (tiled or row-major with
+// d_pad columns) into a dense [n][d] array.
+template <bool TILED>
+__global__ __launch_bounds__(256) void k_export_rows(const uint16_t* __restrict__ src, int64_t first, int n, int d,
+                                                     int d_pad, uint16_t* __restrict__ dst) {
+    const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (t >= (int64_t)n * d) return;
+    const int64_t r = t / d;
+    const int j = (int)(t - r * d);
+    const int64_t off = TILED ? tiled_offset(first + r, j, d_pad >> 5) : (first + r) * (int64_t)d_pad + j;
+    dst[t] = src[off];
+}
+
+hipError_t launch_normalise(const void* in, int dtype, int64_t rows, int64_t rows_pad, int d, int d_pad,
+                            uint16_t* out, int64_t row0, bool tiled, hipStream_t s) {
+    if (rows_pad <= 0) return hipSuccess;
+    const dim3 grid((unsigned)((rows_pad + 3) / 4)), block(256);
+    if (tiled)
+        k_normalise_rows<true><<<grid, block, 0, s>>>(in, dtype, rows, rows_pad, d, d_pad, out, row0);
+    else
+        k_normalise_rows<false><<<grid, block, 0, s>>>(in, dtype, rows, rows_pad, d, d_pad, out, row0);
+    return hipGetLastError();
+}
+
+hipError_t launch_export(const uint16_t* src, int64_t first, int n, int d, int d_pad, uint16_t* dst, bool tiled,
+                         hipStream_t s) {
+    const int64_t total = (int64_t)n * d;
+    if (total <= 0) return hipSuccess;
+    const dim3 grid((unsigned)((total + 255) / 256)), block(256);
+    if (tiled)
+        k_export_rows<true><<<grid, block, 0, s>>>(src, first, n, d, d_pad, dst);
+    else
+        k_export_rows<false><<<grid, block, 0, s>>>(src, first, n, d, d_pad, dst);
+    return hipGetLastError();
+}
+
+}  // namespace lacache

@@ -1,0 +1,110 @@
+// k_verify.hip -- end of stage 1 (merge, threshold) and stage 2 (gather and verify), one wave per query.
+//
+// Stage 1 ends with the best entry over all partial candidates; it is a hit
+// when the clamped similarity is >= tau_q (Section 5.1, cache check).  Only
+// then does stage 2 run (Algorithm 1: the lookahead check sits inside the
+// hit branch): the matched entry's stored prefix -- its embedding row and its
+// first k token IDs (Section 4.2, cache structure <h(x), [h(f_k(x)), f(x)]>)
+// -- is gathered and compared with the query's lookahead.  The check passes
+// on identical tokens, or on a prefix-embedding cosine >= tau_r (Section 5.1,
+// lookahead check).  Decisions: 0 MISS, 1 REJECT, 2 HIT, 3 HIT_EXACT.
+#include "common.hpp"
+#include "launch.hpp"
+
+namespace lacache {
+
+__global__ __launch_bounds__(256) void k_finalize_verify(
+    const uint64_t* __restrict__ part, int P, int B, int n_rows, const void* __restrict__ la, int dtype, int d,
+    const int32_t* __restrict__ la_tok, int k, const uint16_t* __restrict__ emb, int d_pad,
+    const int32_t* __restrict__ tokens, int k_cap, float tau_q, float tau_r, int32_t* __restrict__ idx_out,
+    float* __restrict__ score_out, float* __restrict__ resp_out, int32_t* __restrict__ dec_out) {
+    const int lane = threadIdx.x & 63;
+    const int b = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (b >= B) return;
+    const float qnan = __uint_as_float(0x7FC00000u);
+    if (n_rows <= 0) {
+        if (lane == 0) {
+            idx_out[b] = -1;
+            score_out[b] = qnan;
+            resp_out[b] = qnan;
+            dec_out[b] = 0;
+        }
+        return;
+    }
+    uint64_t m = 0;
+    for (int p = lane; p < P; p += kWave) m = umax64(m, part[(int64_t)b * P + p]);
+    m = wave_max_u64(m);
+    const int32_t i = unpack_idx(m);
+    const float score = fminf(fmaxf(unpack_score(m), -1.0f), 1.0f);
+    // every stored row yields a candidate, so m != 0 here; the range check keeps the gathers in bounds regardless
+    if (m == 0ull || i < 0 || i >= n_rows || !(score >= tau_q)) {
+        if (lane == 0) {
+            idx_out[b] = (m == 0ull) ? -1 : i;
+            score_out[b] = (m == 0ull) ? qnan : score;
+            resp_out[b] = qnan;
+            dec_out[b] = 0;
+        }
+        return;
+    }
+
+    // normalise the lookahead embedding exactly as stored vectors are, and dot it with the entry's prefix row
+    const char* src = (const char*)la + (int64_t)b * d * (dtype == 0 ? 4 : 2);
+    double ss = 0.0;
+    for (int j0 = lane * 8; j0 < d; j0 += 512) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const int j = j0 + e;
+            if (j < d) {
+                const double v = load_in(src, dtype, j);
+                ss += v * v;
+            }
+        }
+    }
+    ss = wave_sum_f64(ss);
+    const double n = __builtin_sqrt(ss);
+    const uint16_t* er = emb + (int64_t)i * d_pad;
+    float acc = 0.0f;
+    if (n != 0.0) {
+        for (int j0 = lane * 8; j0 < d; j0 += 512) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int j = j0 + e;
+                if (j < d) {
+                    const float a = bf16_to_f32(bf16_rne_from_f64(load_in(src, dtype, j) / n));
+                    acc += a * bf16_to_f32(er[j]);  // bf16 x bf16 is exact in float
+                }
+            }
+        }
+    }
+    acc = wave_sum_f32(acc);
+    const float r = fminf(fmaxf(acc, -1.0f), 1.0f);
+
+    // first k tokens: lane j compares token j, 64 at a time
+    bool tok_eq = true;
+    const int32_t* ut = la_tok + (int64_t)b * k;
+    const int32_t* tt = tokens + (int64_t)i * k_cap;
+    for (int j0 = 0; j0 < k; j0 += kWave) {
+        const int j = j0 + lane;
+        const bool differ = (j < k) && (ut[j] != tt[j]);
+        if (__ballot(differ) != 0ull) tok_eq = false;
+    }
+    if (lane == 0) {
+        idx_out[b] = i;
+        score_out[b] = score;
+        resp_out[b] = r;
+        dec_out[b] = tok_eq ? 3 : (r >= tau_r ? 2 : 1);
+    }
+}
+
+hipError_t launch_finalize_verify(const uint64_t* part, int P, int B, int n_rows, const void* la, int dtype, int d,
+                                  const int32_t* la_tok, int k, const uint16_t* emb, int d_pad,
+                                  const int32_t* tokens, int k_cap, float tau_q, float tau_r, int32_t* idx,
+                                  float* score, float* resp_score, int32_t* decision, hipStream_t s) {
+    if (B <= 0) return hipSuccess;
+    k_finalize_verify<<<dim3((B + 3) / 4), dim3(256), 0, s>>>(part, P, B, n_rows, la, dtype, d, la_tok, k, emb,
+                                                              d_pad, tokens, k_cap, tau_q, tau_r, idx, score,
+                                                              resp_score, decision);
+    return hipGetLastError();
+}
+
+}  // namespace lacache

@@ -1,0 +1,290 @@
+// lacache.cpp -- the C ABI (include/lacache.h): handle, argument checks, dispatch onto the caller's stream.
+#include "../../include/lacache.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdlib>
+#include <new>
+#include <utility>
+#include <vector>
+
+#include "launch.hpp"
+
+namespace lacache {
+int stream_max_qg(int d_pad);
+}
+
+using namespace lacache;
+
+struct lacache_s {
+    int device = 0;
+    int64_t cap = 0, cap_pad = 0, size = 0;
+    int d = 0, d_pad = 0, k_cap = 0, dtype = 0, max_batch = 0, mb_pad = 0;
+    int num_cu = 0, b_small = 64;
+    uint16_t* keys = nullptr;  // tiled [cap_pad][d_pad]
+    uint16_t* emb = nullptr;   // row-major [cap][d_pad]
+    int32_t* tokens = nullptr; // [cap][k_cap]
+    uint16_t* qt = nullptr;    // tiled [mb_pad][d_pad] normalised queries
+    uint64_t* part = nullptr;  // [max_batch][kMaxPartials] packed top-1 candidates
+    bool profiling = false;
+    std::vector<std::pair<hipEvent_t, hipEvent_t>> prof;
+};
+
+namespace {
+
+constexpr int64_t kMaxCapacity = (int64_t(1) << 31) - 256;
+constexpr int kRowTile = 256;  // stage-1 GEMM tile: key rows and query rows are padded to it
+
+int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+// Runs `body` with the handle's device current and restores the caller's device.
+struct DeviceGuard {
+    int prev = -1;
+    bool ok = false;
+    explicit DeviceGuard(int dev) {
+        if (hipGetDevice(&prev) != hipSuccess) return;
+        ok = (prev == dev) || hipSetDevice(dev) == hipSuccess;
+    }
+    ~DeviceGuard() {
+        if (ok && prev >= 0) (void)hipSetDevice(prev);
+    }
+};
+
+void free_all(lacache_s* h) {
+    (void)hipFree(h->keys);
+    (void)hipFree(h->emb);
+    (void)hipFree(h->tokens);
+    (void)hipFree(h->qt);
+    (void)hipFree(h->part);
+    for (auto& p : h->prof) {
+        (void)hipEventDestroy(p.first);
+        (void)hipEventDestroy(p.second);
+    }
+    h->prof.clear();
+}
+
+int alloc_zero(void** p, size_t bytes) {
+    if (hipMalloc(p, bytes) != hipSuccess) {
+        *p = nullptr;
+        (void)hipGetLastError();
+        return LACACHE_ENOMEM;
+    }
+    return hipMemset(*p, 0, bytes) == hipSuccess ? LACACHE_OK : LACACHE_EHIP;
+}
+
+void clear_prof(lacache_s* h) {
+    for (auto& p : h->prof) {
+        (void)hipEventDestroy(p.first);
+        (void)hipEventDestroy(p.second);
+    }
+    h->prof.clear();
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* lacache_strerror(int code) {
+    switch (code) {
+        case LACACHE_OK: return "ok";
+        case LACACHE_EINVAL: return "invalid argument";
+        case LACACHE_EFULL: return "cache capacity exceeded";
+        case LACACHE_ENOMEM: return "device allocation failed";
+        case LACACHE_EHIP: return "HIP runtime error";
+        default: return "unknown error code";
+    }
+}
+
+int lacache_create(lacache_t* out, int64_t capacity, int32_t d, int32_t k_cap, lacache_dtype in_dtype,
+                   int32_t max_batch, int32_t device) {
+    if (!out) return LACACHE_EINVAL;
+    *out = nullptr;
+    if (capacity < 1 || capacity > kMaxCapacity || d < 1 || d > 16384 || k_cap < 1 || k_cap > 4096 ||
+        (in_dtype != LACACHE_F32 && in_dtype != LACACHE_BF16) || max_batch < 1 || max_batch > 65536 || device < 0)
+        return LACACHE_EINVAL;
+    int ndev = 0;
+    if (hipGetDeviceCount(&ndev) != hipSuccess) {
+        (void)hipGetLastError();
+        return LACACHE_EHIP;
+    }
+    if (device >= ndev) return LACACHE_EINVAL;
+    DeviceGuard g(device);
+    if (!g.ok) return LACACHE_EHIP;
+
+    lacache_s* h = new (std::nothrow) lacache_s();
+    if (!h) return LACACHE_ENOMEM;
+    h->device = device;
+    h->cap = capacity;
+    h->cap_pad = round_up(capacity, kRowTile);
+    h->d = d;
+    h->d_pad = (int)round_up(d, 128);
+    h->k_cap = k_cap;
+    h->dtype = (int)in_dtype;
+    h->max_batch = max_batch;
+    h->mb_pad = (int)round_up(max_batch, kRowTile);
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, device) != hipSuccess) {
+        delete h;
+        return LACACHE_EHIP;
+    }
+    h->num_cu = prop.multiProcessorCount;
+    if (stream_max_qg(h->d_pad) < 4) h->b_small = 16 * stream_max_qg(h->d_pad);
+
+    int rc = LACACHE_OK;
+    if (rc == LACACHE_OK) rc = alloc_zero((void**)&h->keys, (size_t)h->cap_pad * h->d_pad * 2);
+    if (rc == LACACHE_OK) rc = alloc_zero((void**)&h->emb, (size_t)h->cap * h->d_pad * 2);
+    if (rc == LACACHE_OK) rc = alloc_zero((void**)&h->tokens, (size_t)h->cap * h->k_cap * 4);
+    if (rc == LACACHE_OK) rc = alloc_zero((void**)&h->qt, (size_t)h->mb_pad * h->d_pad * 2);
+    if (rc == LACACHE_OK) rc = alloc_zero((void**)&h->part, (size_t)h->max_batch * kMaxPartials * 8);
+    if (rc == LACACHE_OK && hipDeviceSynchronize() != hipSuccess) rc = LACACHE_EHIP;
+    if (rc != LACACHE_OK) {
+        free_all(h);
+        delete h;
+        return rc;
+    }
+    *out = h;
+    return LACACHE_OK;
+}
+
+int lacache_destroy(lacache_t h) {
+    if (!h) return LACACHE_OK;
+    int rc = LACACHE_OK;
+    {
+        DeviceGuard g(h->device);
+        if (!g.ok || hipDeviceSynchronize() != hipSuccess) rc = LACACHE_EHIP;
+        free_all(h);
+    }
+    delete h;
+    return rc;
+}
+
+int64_t lacache_size(lacache_t h) { return h ? h->size : -1; }
+
+int lacache_insert(lacache_t h, const void* keys, const void* resp_emb, const int32_t* resp_tokens, int32_t n,
+                   int64_t* first_idx, void* stream) {
+    if (!h || n < 0) return LACACHE_EINVAL;
+    if (n == 0) {
+        if (first_idx) *first_idx = h->size;
+        return LACACHE_OK;
+    }
+    if (!keys || !resp_emb || !resp_tokens) return LACACHE_EINVAL;
+    if ((int64_t)n > h->cap - h->size) return LACACHE_EFULL;
+    DeviceGuard g(h->device);
+    if (!g.ok) return LACACHE_EHIP;
+    hipStream_t s = (hipStream_t)stream;
+    const int64_t first = h->size;
+    if (launch_normalise(keys, h->dtype, n, n, h->d, h->d_pad, h->keys, first, true, s) != hipSuccess)
+        return LACACHE_EHIP;
+    if (launch_normalise(resp_emb, h->dtype, n, n, h->d, h->d_pad, h->emb, first, false, s) != hipSuccess)
+        return LACACHE_EHIP;
+    if (hipMemcpyAsync(h->tokens + first * h->k_cap, resp_tokens, (size_t)n * h->k_cap * 4,
+                       hipMemcpyDeviceToDevice, s) != hipSuccess)
+        return LACACHE_EHIP;
+    h->size += n;
+    if (first_idx) *first_idx = first;
+    return LACACHE_OK;
+}
+
+static int lookup_chunk(lacache_t h, const char* queries, const char* la, const int32_t* la_tok, int B, float tau_q,
+                        float tau_r, int k, int32_t* idx, float* score, float* resp, int32_t* dec, hipStream_t s) {
+    const int n_rows = (int)h->size;
+    int P = 0;
+    if (n_rows > 0) {
+        const bool small = B <= h->b_small;
+        const int64_t rows_pad = small ? round_up(B, 16) : round_up(B, kRowTile);
+        if (launch_normalise(queries, h->dtype, B, rows_pad, h->d, h->d_pad, h->qt, 0, true, s) != hipSuccess)
+            return LACACHE_EHIP;
+        hipEvent_t e0 = nullptr, e1 = nullptr;
+        if (h->profiling) {
+            if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) return LACACHE_EHIP;
+            h->prof.emplace_back(e0, e1);
+            if (hipEventRecord(e0, s) != hipSuccess) return LACACHE_EHIP;
+        }
+        hipError_t e = small ? launch_stage1_stream(h->keys, h->qt, B, n_rows, h->d_pad, h->part, h->num_cu, &P, s)
+                             : launch_stage1_gemm(h->keys, h->qt, B, n_rows, h->d_pad, h->part, h->num_cu, &P, s);
+        if (e != hipSuccess) return LACACHE_EHIP;
+        if (h->profiling && hipEventRecord(e1, s) != hipSuccess) return LACACHE_EHIP;
+    }
+    if (launch_finalize_verify(h->part, P, B, n_rows, la, h->dtype, h->d, la_tok, k, h->emb, h->d_pad, h->tokens,
+                               h->k_cap, tau_q, tau_r, idx, score, resp, dec, s) != hipSuccess)
+        return LACACHE_EHIP;
+    return LACACHE_OK;
+}
+
+int lacache_lookup(lacache_t h, const void* queries, const void* lookahead_emb, const int32_t* lookahead_tokens,
+                   int32_t B, float tau_q, float tau_r, int32_t k, int32_t* idx, float* score, float* resp_score,
+                   int32_t* decision, void* stream) {
+    if (!h || B < 0 || k < 1 || k > h->k_cap || !std::isfinite(tau_q) || !std::isfinite(tau_r))
+        return LACACHE_EINVAL;
+    if (B == 0) return LACACHE_OK;
+    if (!queries || !lookahead_emb || !lookahead_tokens || !idx || !score || !resp_score || !decision)
+        return LACACHE_EINVAL;
+    DeviceGuard g(h->device);
+    if (!g.ok) return LACACHE_EHIP;
+    const size_t esz = h->dtype == LACACHE_F32 ? 4 : 2;
+    for (int b0 = 0; b0 < B; b0 += h->max_batch) {
+        const int nb = (B - b0) < h->max_batch ? (B - b0) : h->max_batch;
+        const int rc = lookup_chunk(h, (const char*)queries + (size_t)b0 * h->d * esz,
+                                    (const char*)lookahead_emb + (size_t)b0 * h->d * esz,
+                                    lookahead_tokens + (size_t)b0 * k, nb, tau_q, tau_r, k, idx + b0, score + b0,
+                                    resp_score + b0, decision + b0, (hipStream_t)stream);
+        if (rc != LACACHE_OK) return rc;
+    }
+    return LACACHE_OK;
+}
+
+int lacache_export(lacache_t h, int64_t first, int32_t n, uint16_t* keys_bf16, uint16_t* emb_bf16, int32_t* tokens,
+                   void* stream) {
+    if (!h || first < 0 || n < 0 || first + n > h->size) return LACACHE_EINVAL;
+    if (n == 0) return LACACHE_OK;
+    DeviceGuard g(h->device);
+    if (!g.ok) return LACACHE_EHIP;
+    hipStream_t s = (hipStream_t)stream;
+    if (keys_bf16 && launch_export(h->keys, first, n, h->d, h->d_pad, keys_bf16, true, s) != hipSuccess)
+        return LACACHE_EHIP;
+    if (emb_bf16 && launch_export(h->emb, first, n, h->d, h->d_pad, emb_bf16, false, s) != hipSuccess)
+        return LACACHE_EHIP;
+    if (tokens && hipMemcpyAsync(tokens, h->tokens + first * h->k_cap, (size_t)n * h->k_cap * 4,
+                                 hipMemcpyDeviceToDevice, s) != hipSuccess)
+        return LACACHE_EHIP;
+    return LACACHE_OK;
+}
+
+int lacache_set_small_batch(lacache_t h, int32_t b_small) {
+    if (!h || b_small < 0 || b_small > 16 * stream_max_qg(h->d_pad)) return LACACHE_EINVAL;
+    h->b_small = b_small;
+    return LACACHE_OK;
+}
+
+int lacache_profile(lacache_t h, int32_t enable) {
+    if (!h) return LACACHE_EINVAL;
+    DeviceGuard g(h->device);
+    clear_prof(h);
+    h->profiling = enable != 0;
+    return LACACHE_OK;
+}
+
+int lacache_profile_read(lacache_t h, double* stage1_ms, int64_t* lookups) {
+    if (!h || !stage1_ms || !lookups) return LACACHE_EINVAL;
+    DeviceGuard g(h->device);
+    if (!g.ok) return LACACHE_EHIP;
+    double total = 0.0;
+    int64_t cnt = 0;
+    int rc = LACACHE_OK;
+    for (auto& p : h->prof) {
+        float ms = 0.f;
+        if (hipEventSynchronize(p.second) != hipSuccess || hipEventElapsedTime(&ms, p.first, p.second) != hipSuccess) {
+            rc = LACACHE_EHIP;
+            break;
+        }
+        total += ms;
+        ++cnt;
+    }
+    clear_prof(h);
+    *stage1_ms = total;
+    *lookups = cnt;
+    return rc;
+}
+
+}  // extern "C"

@@ -1,0 +1,41 @@
+// launch.hpp -- host-side launchers of the gfx950 kernels (called by the C ABI in lacache.cpp).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace lacache {
+
+// Normalise `rows` input rows (dtype 0 f32 / 1 bf16, row-major [rows][d]) and
+// store them as bfloat16 at destination rows row0 .. row0+rows-1, zero-filling
+// up to rows_pad rows and d_pad columns; `tiled` selects the key layout,
+// otherwise row-major [.][d_pad].
+hipError_t launch_normalise(const void* in, int dtype, int64_t rows, int64_t rows_pad, int d, int d_pad,
+                            uint16_t* out, int64_t row0, bool tiled, hipStream_t s);
+
+// Dense [n][d] copy of stored rows first .. first+n-1.
+hipError_t launch_export(const uint16_t* src, int64_t first, int n, int d, int d_pad, uint16_t* dst, bool tiled,
+                         hipStream_t s);
+
+// Stage 1, bandwidth-bound path: queries qt (tiled, B <= 64 rows, zero-padded
+// to a multiple of 16) against n_rows tiled keys.  Writes, for every query b
+// and every workgroup p of the launch, the packed top-1 candidate
+// part[b * P + p] (P <= kMaxPartials).  Returns the number of partials P through *P_out.
+hipError_t launch_stage1_stream(const uint16_t* keys, const uint16_t* qt, int B, int n_rows, int d_pad,
+                                uint64_t* part, int num_cu, int* P_out, hipStream_t s);
+
+// Stage 1, compute-bound path (matrix-core GEMM with a fused row argmax):
+// queries qt (tiled, rows padded to a multiple of 256) against n_rows keys.
+hipError_t launch_stage1_gemm(const uint16_t* keys, const uint16_t* qt, int B, int n_rows, int d_pad,
+                              uint64_t* part, int num_cu, int* P_out, hipStream_t s);
+
+// Merge the P partial candidates of each query, threshold, and run stage 2 on hits.
+hipError_t launch_finalize_verify(const uint64_t* part, int P, int B, int n_rows, const void* la,
+                                  int dtype, int d, const int32_t* la_tok, int k, const uint16_t* emb, int d_pad,
+                                  const int32_t* tokens, int k_cap, float tau_q, float tau_r, int32_t* idx,
+                                  float* score, float* resp_score, int32_t* decision, hipStream_t s);
+
+// Most partials a stage-1 launch may write per query.
+constexpr int kMaxPartials = 1024;
+
+}  // namespace lacache

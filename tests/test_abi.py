@@ -1,0 +1,93 @@
+"""The C-ABI library: it builds, loads, exports every declared entry point, and rejects bad arguments
+before touching a device (no GPU needed)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "lacache.h")
+LIB = os.path.join(ROOT, "paper_2608_01718_amd", "liblacache.so")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(LIB):
+        from paper_2608_01718_amd import build as b
+        b.build()
+    return ctypes.CDLL(LIB)
+
+
+def declared():
+    txt = open(HEADER).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(lacache_[a-z_]+)\s*\(", txt)))
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = declared()
+    assert len(names) >= 10
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_binding_mirrors_the_abi():
+    import paper_2608_01718_amd as m
+    assert sorted(m.EXPORTED) == declared()
+    for n in declared():
+        assert callable(getattr(m, n)), n
+
+
+def test_argument_checks_before_any_device_work(lib):
+    P = ctypes.c_void_p
+    lib.lacache_create.argtypes = [ctypes.POINTER(P), ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int,
+                                   ctypes.c_int32, ctypes.c_int32]
+    h = P()
+    EINVAL = -1
+    bad = [(0, 64, 8, 1, 16, 0), (-5, 64, 8, 1, 16, 0), (2 ** 31, 64, 8, 1, 16, 0), (10, 0, 8, 1, 16, 0),
+           (10, 20000, 8, 1, 16, 0), (10, 64, 0, 1, 16, 0), (10, 64, 5000, 1, 16, 0), (10, 64, 8, 2, 16, 0),
+           (10, 64, 8, 1, 0, 0), (10, 64, 8, 1, 70000, 0), (10, 64, 8, 1, 16, -1)]
+    for args in bad:
+        assert lib.lacache_create(ctypes.byref(h), *args) == EINVAL, args
+        assert not h.value
+    assert lib.lacache_create(None, 10, 64, 8, 1, 16, 0) == EINVAL
+    lib.lacache_size.argtypes = [P]
+    lib.lacache_size.restype = ctypes.c_int64
+    assert lib.lacache_size(None) == -1
+    lib.lacache_lookup.argtypes = [P] * 5 + [ctypes.c_float, ctypes.c_float, ctypes.c_int32] + [P] * 5
+    assert lib.lacache_lookup(None, None, None, None, 0, 0.5, 0.5, 1, None, None, None, None, None) == EINVAL
+    lib.lacache_insert.argtypes = [P, P, P, P, ctypes.c_int32, P, P]
+    assert lib.lacache_insert(None, None, None, None, 0, None, None) == EINVAL
+    lib.lacache_export.argtypes = [P, ctypes.c_int64, ctypes.c_int32, P, P, P, P]
+    assert lib.lacache_export(None, 0, 0, None, None, None, None) == EINVAL
+    assert lib.lacache_destroy(None) == 0
+    lib.lacache_set_small_batch.argtypes = [P, ctypes.c_int32]
+    assert lib.lacache_set_small_batch(None, 16) == EINVAL
+    lib.lacache_profile_read.argtypes = [P, P, P]
+    assert lib.lacache_profile_read(None, None, None) == EINVAL
+    lib.lacache_strerror.restype = ctypes.c_char_p
+    assert lib.lacache_strerror(-2) == b"cache capacity exceeded"
+    assert lib.lacache_strerror(12345) == b"unknown error code"
+
+
+def test_store_layout_offsets_match_the_mfma_fragment():
+    """The tiled key layout: lane l of a wave reading 16 bytes at l*16 within a 1 KiB chunk gets row l%16
+    and columns 8*(l//16) .. +7 of a 16 x 32 block (host-side arithmetic check of the layout formula)."""
+    src = open(os.path.join(ROOT, "paper_2608_01718_amd", "csrc", "common.hpp")).read()
+    assert "((row >> 4) * kc + (col >> 5)) * 512 + (((col >> 3) & 3) * 16 + (row & 15)) * 8 + (col & 7)" in src
+
+    def off(row, col, kc):
+        return ((row >> 4) * kc + (col >> 5)) * 512 + (((col >> 3) & 3) * 16 + (row & 15)) * 8 + (col & 7)
+    kc = 24
+    seen = set()
+    for row in range(48):
+        for col in range(768):
+            o = off(row, col, kc)
+            assert o not in seen
+            seen.add(o)
+            chunk, within = divmod(o, 512)
+            lane, e = divmod(within, 8)
+            assert chunk == (row // 16) * kc + col // 32
+            assert lane % 16 == row % 16 and 8 * (lane // 16) + e == col % 32
+    assert seen == set(range(48 * 768))

@@ -1,0 +1,279 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle on the same seeded inputs."""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from tests.compare import compare
+from tests.gpu_util import gpu_cache, gpu_lookup, oracle_store, sample_rows, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def lc():
+    import torch
+    assert torch.cuda.is_available()
+    import paper_2608_01718_amd as m
+    return m
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def _run(lc, sp, w=None, call_b=None, b_small=None, rows=None, insert_chunk=None, max_batch=4096):
+    w = w or synth.generate(sp)
+    say(f"[case] {sp.name} N={sp.N} d={sp.d} B={w.queries.shape[0]} k={sp.k} call_b={call_b} b_small={b_small}")
+    c = gpu_cache(lc, sp, w.keys, w.emb, w.tokens, max_batch=max_batch, insert_chunk=insert_chunk)
+    if b_small is not None:
+        c.set_small_batch(b_small)
+    g = gpu_lookup(c, w.queries, w.la_emb, w.la_tok, sp.tau_q, sp.tau_r, sp.k, call_b)
+    kq, eq, tok = oracle_store(sp, w.keys, w.emb, w.tokens)
+    qq = oracle.quantise(w.queries, sp.in_dtype)
+    aq = oracle.quantise(w.la_emb, sp.in_dtype)
+    u = np.ascontiguousarray(w.la_tok[:, :sp.k])
+    rows = np.arange(w.queries.shape[0]) if rows is None else rows
+    o = oracle.lookup(kq, eq, tok, qq[rows], aq[rows], u[rows], sp.tau_q, sp.tau_r, sp.k)
+    stats = compare(g, o, kq, eq, tok, qq, aq, u, sp.tau_q, sp.tau_r, sp.k, rows)
+    say(f"[ok] {sp.name}: {stats}")
+    c.close()
+    return w, g, o, stats
+
+
+def test_store_matches_oracle_quantisation(lc):
+    for name, N in [("tiny", 3000), ("mid", 3000), ("mid_paper", 1000)]:
+        sp = synth.spec(name, N=N)
+        w = synth.generate(sp)
+        c = gpu_cache(lc, sp, w.keys, w.emb, w.tokens, capacity=N + 5, insert_chunk=777)
+        k, e, t = (x.cpu().numpy() for x in c.export(0, N))
+        kq, eq, tok = oracle_store(sp, w.keys, w.emb, w.tokens)
+        for got, want in ((k.view(np.uint16), kq), (e.view(np.uint16), eq)):
+            diff = got != want
+            # the float64 normalisation may sum in another order; a 1-ulp flip at a rounding tie is allowed
+            assert diff.mean() <= 1e-3
+            ulp = np.abs(got.astype(np.int32) - want.astype(np.int32))
+            assert np.all(ulp[diff] <= 1)
+        np.testing.assert_array_equal(t, tok)
+        c.close()
+
+
+@pytest.mark.parametrize("name", ["tiny", "mid", "mid_paper"])
+def test_parity_full_config(lc, name):
+    _run(lc, synth.spec(name))
+
+
+def test_parity_serve_small_reduced(lc):
+    sp = synth.spec("serve_small", N=60_000, B=256)
+    _run(lc, sp, call_b=synth.SERVE_SMALL_CALL_B)
+
+
+def test_parity_serve_large_reduced(lc):
+    sp = synth.spec("serve_large", N=40_000, n_dup=200, n_dup_queries=64)
+    w, g, o, _ = _run(lc, sp)
+    # duplicate-aimed benign queries resolve to the earlier copy and are served from its prefix
+    dq = np.nonzero(np.isin(w.target, w.dup_pairs[:, 0]) & (w.cls == synth.CLS_BENIGN))[0]
+    assert len(dq) >= 32
+    np.testing.assert_array_equal(g["idx"][dq], w.target[dq])
+    np.testing.assert_array_equal(g["decision"][dq], oracle.HIT_EXACT)
+
+
+def test_parity_large_clustered_reduced(lc):
+    sp = synth.spec("large", N=30_000, B=512)
+    _run(lc, sp)
+
+
+def test_parity_serve_small_full_size_sampled(lc):
+    sp = synth.spec("serve_small", B=256)
+    w = synth.generate(sp)
+    rows = sample_rows(w.cls, w.target, 48)
+    _run(lc, sp, w=w, call_b=synth.SERVE_SMALL_CALL_B, rows=rows)
+
+
+def test_parity_serve_large_full_size_sampled(lc):
+    sp = synth.spec("serve_large")
+    w = synth.generate(sp)
+    dq = np.nonzero(np.isin(w.target, w.dup_pairs[:, 0]) & (w.cls == synth.CLS_BENIGN))[0][:16]
+    rows = np.unique(np.concatenate([sample_rows(w.cls, w.target, 48), dq]))
+    _, g, _, _ = _run(lc, sp, w=w, rows=rows)
+    # the whole batch: every duplicate-aimed query resolves to the earlier copy
+    dq = np.nonzero(np.isin(w.target, w.dup_pairs[:, 0]) & (w.cls == synth.CLS_BENIGN))[0]
+    np.testing.assert_array_equal(g["idx"][dq], w.target[dq])
+    # synthetic hit-rate analogues over the whole batch: benign plants served, collisions rejected
+    ben = w.cls == synth.CLS_BENIGN
+    col = w.cls == synth.CLS_COLLISION
+    assert np.all(np.isin(g["decision"][ben], [oracle.HIT, oracle.HIT_EXACT]))
+    assert np.all(g["decision"][col] == oracle.REJECT)
+    assert np.all(g["decision"][w.cls == synth.CLS_MISS] == oracle.MISS)
+
+
+# ------------------------------------------------------------------------------------------- edge cases
+
+
+def _edge(lc, N, d, B, k_cap, k, dtype=oracle.F32, seed=0, b_small=None, neg=False, zero_rows=(), dup=0,
+          zero_queries=()):
+    rng = np.random.default_rng(seed)
+    sp = synth.Spec("edge", N, d, dtype, k_cap, 50, B, 0, 0, 0, 0, 0.3, 0.2, k, seed)
+    dt = np.float32
+    keys = rng.standard_normal((N, d)).astype(dt)
+    if neg:
+        # every key close to one direction, every query opposite to it: all real scores are near -1
+        keys = (rng.standard_normal(d) + 0.2 * keys).astype(dt)
+    emb = rng.standard_normal((N, d)).astype(dt)
+    tok = rng.integers(0, 50, (N, k_cap), dtype=np.int32)
+    for r in zero_rows:
+        if r < N:
+            keys[r] = 0
+    if dup and N > 2:
+        keys[rng.integers(N // 2, N, dup)] = keys[rng.integers(0, N // 2, dup)]
+    q = rng.standard_normal((B, d)).astype(dt)
+    pick = rng.integers(0, max(N, 1), B)
+    if N:
+        q[: B // 2] = keys[pick[: B // 2]] + 0.05 * rng.standard_normal((B // 2, d)).astype(dt)
+        if neg:
+            q[:] = -keys[pick]
+    for r in zero_queries:
+        q[r] = 0
+    a = rng.standard_normal((B, d)).astype(dt)
+    u = rng.integers(0, 50, (B, k), dtype=np.int32)
+    if N:
+        u[: B // 4] = tok[pick[: B // 4], :k]
+        a[B // 4: B // 2] = emb[pick[B // 4: B // 2]]
+    if dtype == oracle.BF16:
+        keys, emb, q, a = (synth.to_bf16_bits(x) for x in (keys, emb, q, a))
+    w = synth.Workload(sp, keys, emb, tok, q, a, u, np.zeros(B, np.int32), np.full(B, -1), np.full(B, np.nan),
+                       np.zeros((0, 2), np.int64))
+    say(f"[edge] N={N} d={d} B={B} k_cap={k_cap} k={k} dtype={dtype} b_small={b_small} neg={neg}")
+    c = gpu_cache(lc, sp, keys, emb, tok, capacity=max(N, 1) + 3)
+    if b_small is not None:
+        c.set_small_batch(b_small)
+    g = gpu_lookup(c, q, a, u, sp.tau_q, sp.tau_r, k)
+    kq, eq, tq = oracle_store(sp, keys, emb, tok)
+    qq, aq = oracle.quantise(q, dtype), oracle.quantise(a, dtype)
+    o = oracle.lookup(kq, eq, tq, qq, aq, u, sp.tau_q, sp.tau_r, k)
+    compare(g, o, kq, eq, tq, qq, aq, u, sp.tau_q, sp.tau_r, k)
+    c.close()
+    return w, g, o
+
+
+@pytest.mark.parametrize("N,d,B,k_cap,k", [
+    (1, 64, 5, 1, 1),          # a single entry
+    (17, 64, 16, 8, 8),        # one live row in the last 16-row group
+    (255, 100, 17, 150, 150),  # d not a multiple of 128, k > 64 (two ballot rounds), ragged B
+    (257, 384, 63, 20, 1),     # k = 1
+    (1000, 384, 65, 64, 64),   # B just past the small-batch limit
+    (4097, 768, 300, 16, 16),  # ragged everything on the large-batch path
+    (300, 1024, 1, 32, 32),    # B = 1
+])
+@pytest.mark.parametrize("dtype", [oracle.F32, oracle.BF16])
+def test_edge_shapes(lc, N, d, B, k_cap, k, dtype):
+    _edge(lc, N, d, B, k_cap, k, dtype)
+
+
+@pytest.mark.parametrize("b_small", [0, 64])
+def test_all_negative_scores_never_pick_padding(lc, b_small):
+    # every real score is negative; padded rows (zeros) would score 0 if they were not masked
+    for N in (1, 17, 250):
+        _, g, o = _edge(lc, N, 64, 40, 4, 4, neg=True, b_small=b_small, seed=N)
+        assert np.all(g["idx"] < N) and np.all(g["score"] < 0)
+
+
+def test_zero_vectors_and_duplicates(lc):
+    _edge(lc, 500, 128, 70, 8, 8, zero_rows=(0, 3, 499), dup=40)
+    # a zero query scores 0 against everything: index 0, score 0
+    _, g, _ = _edge(lc, 50, 32, 4, 2, 2, seed=9, zero_queries=(1, 3))
+    assert g["idx"][1] == 0 and g["score"][1] == 0 and g["idx"][3] == 0 and g["score"][3] == 0
+
+
+def test_empty_cache(lc):
+    import torch
+    c = lc.LaCache(10, 32, 4, oracle.F32, 16, 0)
+    q = torch.randn(5, 32, device="cuda")
+    t = torch.zeros(5, 4, dtype=torch.int32, device="cuda")
+    idx, score, resp, dec = (x.cpu().numpy() for x in c.lookup(q, q, t, 0.5, 0.5, 4))
+    assert np.all(idx == -1) and np.all(np.isnan(score)) and np.all(np.isnan(resp)) and np.all(dec == 0)
+    assert np.all(resp.view(np.uint32) == 0x7FC00000)
+    c.close()
+
+
+def test_determinism_and_paths_agree(lc):
+    import torch
+    sp = synth.spec("mid", N=20_000, B=64)
+    w = synth.generate(sp)
+    c = gpu_cache(lc, sp, w.keys, w.emb, w.tokens)
+    runs = [gpu_lookup(c, w.queries, w.la_emb, w.la_tok, sp.tau_q, sp.tau_r, sp.k) for _ in range(5)]
+    for r in runs[1:]:
+        for n in runs[0]:
+            np.testing.assert_array_equal(r[n].view(np.uint32) if r[n].dtype == np.float32 else r[n],
+                                          runs[0][n].view(np.uint32) if runs[0][n].dtype == np.float32
+                                          else runs[0][n])
+    c.set_small_batch(0)
+    g = gpu_lookup(c, w.queries, w.la_emb, w.la_tok, sp.tau_q, sp.tau_r, sp.k)
+    s = runs[0]
+    assert np.all(np.abs(g["score"] - s["score"]) <= 1e-5)
+    np.testing.assert_array_equal(g["idx"], s["idx"])
+    np.testing.assert_array_equal(g["decision"], s["decision"])
+    c.close()
+    torch.cuda.synchronize()
+
+
+def test_interleaved_inserts(lc):
+    """A query planted near an entry is a miss before that entry is inserted and a hit after it."""
+    sp = synth.spec("large", N=12_288, B=256)
+    keys, emb, tok = synth.entries(sp, 0, sp.N)
+    base = 8192
+    c = gpu_cache(lc, sp, keys[:base], emb[:base], tok[:base], capacity=sp.N, insert_chunk=4096)
+    late = synth.queries(sp, keys, emb, tok, np.zeros((0, 2), np.int64), B=256, N=sp.N, stream_chunk=7)
+    aimed_late = (late["target"] >= base) & (late["cls"] == synth.CLS_BENIGN)
+    assert aimed_late.sum() > 10
+    g0 = gpu_lookup(c, late["queries"], late["la_emb"], late["la_tok"], sp.tau_q, sp.tau_r, sp.k)
+    assert np.all(g0["idx"][aimed_late] < base)
+    assert np.all(g0["decision"][aimed_late] == oracle.MISS)
+    for r0 in range(base, sp.N, 4096):
+        assert c.insert(to_dev(keys[r0:r0 + 4096]), to_dev(emb[r0:r0 + 4096]), to_dev(tok[r0:r0 + 4096])) == r0
+    g1 = gpu_lookup(c, late["queries"], late["la_emb"], late["la_tok"], sp.tau_q, sp.tau_r, sp.k)
+    np.testing.assert_array_equal(g1["idx"][aimed_late], late["target"][aimed_late])
+    assert np.all(g1["decision"][aimed_late] == oracle.HIT_EXACT)
+    kq, eq, tq = oracle_store(sp, keys, emb, tok)
+    qq, aq = oracle.quantise(late["queries"], sp.in_dtype), oracle.quantise(late["la_emb"], sp.in_dtype)
+    u = np.ascontiguousarray(late["la_tok"][:, :sp.k])
+    o = oracle.lookup(kq, eq, tq, qq, aq, u, sp.tau_q, sp.tau_r, sp.k)
+    compare(g1, o, kq, eq, tq, qq, aq, u, sp.tau_q, sp.tau_r, sp.k)
+    c.close()
+
+
+def test_errors_with_live_handle(lc):
+    import torch
+    c = lc.LaCache(100, 16, 4, oracle.F32, 8, 0)
+    x = torch.randn(60, 16, device="cuda")
+    t = torch.zeros(60, 4, dtype=torch.int32, device="cuda")
+    assert c.insert(x, x, t) == 0
+    with pytest.raises(lc.LaCacheError) as e:
+        c.insert(x, x, t)                       # 60 + 60 > 100: nothing inserted
+    assert e.value.code == lc.EFULL and c.size() == 60
+    q = x[:4]
+    with pytest.raises(lc.LaCacheError) as e:
+        c.lookup(q, q, torch.zeros(4, 5, dtype=torch.int32, device="cuda"), 0.5, 0.5, 5)   # k > k_cap
+    assert e.value.code == lc.EINVAL
+    with pytest.raises(lc.LaCacheError) as e:
+        c.lookup(q, q, t[:4], float("nan"), 0.5, 4)
+    assert e.value.code == lc.EINVAL
+    with pytest.raises(lc.LaCacheError):
+        c.lookup(q, q, t[:4], 0.5, float("inf"), 4)
+    with pytest.raises(lc.LaCacheError):
+        c.set_small_batch(65)
+    with pytest.raises(ValueError):
+        c.lookup(q.double(), q, t[:4], 0.5, 0.5, 4)
+    # a lookup with more queries than max_batch runs in chunks and matches chunk-by-chunk lookups
+    q2 = torch.randn(21, 16, device="cuda")
+    t2 = torch.zeros(21, 4, dtype=torch.int32, device="cuda")
+    whole = [z.cpu() for z in c.lookup(q2, q2, t2, 0.1, 0.1, 4)]
+    parts = [[z.cpu() for z in c.lookup(q2[i:i + 8], q2[i:i + 8], t2[i:i + 8], 0.1, 0.1, 4)] for i in (0, 8, 16)]
+    for j in range(4):
+        assert torch.equal(whole[j].view(torch.int32), torch.cat([p[j] for p in parts]).view(torch.int32))
+    c.close()
