@@ -96,7 +96,11 @@ def run_workload(name, steps, warmup, lc, torch, synth, traffic_db, want_cpu):
     c.profile(False)
     k_avg = k_ms / max(k_n, 1)
 
-    # decisions of every query of the pool (synthetic hit-rate analogues of the paper's BHR / AHR)
+    # one more pass over every call of the pool, then the decisions of all its queries
+    # (synthetic analogues of the paper's benign and attack hit rates)
+    for i in range(n_calls):
+        step(i)
+    torch.cuda.synchronize()
     dec = np.concatenate([outs[i][3].cpu().numpy() for i in range(n_calls)])
     ben, col = w.cls == synth.CLS_BENIGN, w.cls == synth.CLS_COLLISION
     served = np.isin(dec, [2, 3])
