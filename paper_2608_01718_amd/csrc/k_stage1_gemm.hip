@@ -7,18 +7,25 @@
 // that belongs on the matrix cores -- but only its row maxima are needed, so
 // the B x N score matrix never leaves registers.
 //
-// Tiling: a workgroup (4 waves, 2 x 2) owns a tile of 256 queries and walks a
-// contiguous range of 256-key tiles.  For each key tile it streams d in steps
-// of 64 through double-buffered LDS (keys and queries arrive as 1 KiB chunks of
-// the tiled layout, one coalesced wave access each); every wave computes a
-// 128-key x 128-query block with v_mfma_f32_32x32x16_bf16 (keys are the row
-// operand, so a lane's 16 accumulators are 16 keys of one query).  At the end
-// of a key tile each lane reduces its 64 keys per query in registers and
-// updates a running (best score, index); a scan for the index runs only when
-// some lane improved.  Key rows are visited in increasing order and only a
-// strictly larger score replaces the best, so ties keep the lowest index.
-// Rows past the stored entry count are masked in the last tile.  At the end
-// the workgroup writes one packed candidate per query for its key range.
+// Tiling: a workgroup of 8 waves owns a tile of 256 queries and walks a
+// contiguous range of 256-key tiles.  Each key tile is consumed in stages of
+// 32 columns: a stage (16 KiB of keys + 16 KiB of queries, 1 KiB chunks of the
+// tiled store layout) is copied by buffer loads straight into one of four LDS
+// buffers, three stages ahead of the one being multiplied, so the copies have
+// three stage-times to arrive from L2 or HBM.  Waves are arranged 2 (key
+// halves of 128) x 4 (query quarters of 64); a wave multiplies its 128 x 64
+// block with v_mfma_f32_32x32x16_bf16, keys as the row operand, so a lane's 16
+// accumulators per fragment are 16 keys of one query.  After the last stage of
+// a key tile each lane reduces its 64 keys per query in registers and updates
+// a running (best score, index); the scan for the index runs only when some
+// lane of the wave improved.  Key rows are visited in increasing order and
+// only a strictly larger score replaces the best, so ties keep the lowest
+// index.  The one partial key tile (rows beyond the entry count are zero
+// padding and must not win) is handled by a separate, masked instantiation.
+// At the end each workgroup writes one packed candidate per query.
+#include <cstdlib>
+#include <type_traits>
+
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -26,18 +33,20 @@ namespace lacache {
 
 namespace {
 
-constexpr int kTile = 256;     // queries and keys per workgroup tile
-constexpr int kChunks = 32;    // 1 KiB chunks per operand per stage: (256 / 16 rows) x (64 / 32 cols)
-constexpr int kStageBytes = 2 * kChunks * 1024;  // keys + queries
-constexpr int kWaves = 8;      // 2 key halves x 4 query quarters
-constexpr int QF = 2;          // 32-query MFMA fragments per wave
+constexpr int kTile = 256;                           // queries and keys per workgroup tile
+constexpr int kWaves = 8;                            // 2 key halves x 4 query quarters
+constexpr int QF = 2;                                // 32-query MFMA fragments per wave
+constexpr int kNBuf = 4;                             // LDS stage buffers (prefetch distance kNBuf - 1)
+constexpr int kChunks = 16;                          // 1 KiB chunks per operand per stage (256 rows x 32 cols)
+constexpr int kStageBytes = 2 * kChunks * 1024;      // keys + queries
+constexpr int kPerWave = kChunks / kWaves;           // chunks of each operand a wave copies per stage
 
-// byte offset in an operand's LDS stage of the 32x32x16 fragment for lane l:
-// rows [row0, row0 + 32), the 16 columns of substep s (0..3) of the 64-column stage
+// byte offset, inside one operand's stage, of the 32x32x16 fragment read by lane l:
+// rows [row0, row0 + 32), columns 16 s .. 16 s + 15 of the 32-column stage
 __device__ inline int frag_offset(int row0, int s, int lane) {
     const int g = (row0 >> 4) + ((lane & 31) >> 4);  // 16-row group inside the 256-row tile
-    const int c = ((s & 1) << 1) + (lane >> 5);      // 8-column chunk inside the 32-column block
-    return ((g * 2 + (s >> 1)) * 64 + c * 16 + (lane & 15)) * 16;
+    const int c = (s << 1) + (lane >> 5);            // 8-column chunk inside the 32-column block
+    return (g * 64 + c * 16 + (lane & 15)) * 16;
 }
 
 // Buffer resource over `bytes` bytes at `base`: loads through it outside [0, bytes) return zeros
@@ -53,161 +62,165 @@ __device__ inline void buffer_to_lds16(__amdgpu_buffer_rsrc_t r, uint32_t voff, 
                                              soff, 0, 0);
 }
 
-__device__ inline void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+// Wait until at most `stages` stages of this wave's copies are still in flight.
+__device__ inline void wait_stages_in_flight(int stages) {
+    static_assert(2 * kPerWave == 4, "vmcnt immediates below assume 4 copies per wave per stage");
+    if (stages >= 2)
+        asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+    else if (stages == 1)
+        asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+    else
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+}
 
 }  // namespace
 
 // MASKED = false: key tiles [0, n_ktiles) are all full; they are split into n_ranges contiguous ranges and
 // range r writes partial slot r.  MASKED = true: the single partial tile n_ktiles (rows n_ktiles*256 ..
-// n_rows-1), written to partial slot `slot`.  P is the partial stride of a query.
+// n_rows-1), written to partial slot `slot`.  P is the partial stride of a query.  xq selects the XCD
+// placement of the workgroups (below); it requires n_qtiles % xq == 0 and n_ranges % (8 / xq) == 0.
 template <bool MASKED>
 __global__ __launch_bounds__(512, 1) void k_stage1_gemm(const u32x4* __restrict__ keys, const u32x4* __restrict__ qt,
                                                         int kc, int n_rows, int B, int n_qtiles, int n_ktiles,
-                                                        int n_ranges, int slot, int P, uint64_t* __restrict__ part) {
+                                                        int n_ranges, int slot, int P, int xq,
+                                                        uint64_t* __restrict__ part) {
     extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
     const int tid = threadIdx.x, lane = tid & 63;
     const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform, kept in scalar registers
-    const int wk = wid & 1, wq = wid >> 1;  // key half (128 keys), query quarter (64 queries)
+    const int wk = wid & 1, wq = wid >> 1;                     // key half (128 keys), query quarter (64)
 
-    // workgroup -> (query tile, key range); consecutive workgroups take consecutive query tiles of one key
-    // range, so the key tiles they share are fetched from HBM once and then served by L2.
-    const int wg = blockIdx.x;
-    const int qtile = wg % n_qtiles;
-    const int range = wg / n_qtiles;
+    // workgroup -> (query tile, key range).  Dispatch is round-robin over the 8 XCDs (one L2 each).  With
+    // xq > 0 the XCDs form xq query groups x (8 / xq) key parts: XCD x serves the query tiles of group
+    // x % xq (small enough to stay in its L2) against key part x / xq, and consecutive workgroups of an XCD
+    // take consecutive query tiles of one key range, so that range's keys come into that L2 once.
+    int qtile, range;
+    if (xq > 0) {
+        const int xcd = blockIdx.x % 8, j = blockIdx.x / 8;
+        const int qpg = n_qtiles / xq, rpp = n_ranges / (8 / xq);
+        qtile = (xcd % xq) * qpg + j % qpg;
+        range = (xcd / xq) * rpp + j / qpg;
+    } else {
+        qtile = blockIdx.x % n_qtiles;
+        range = blockIdx.x / n_qtiles;
+    }
     const int kt0 = MASKED ? n_ktiles : (int)((int64_t)range * n_ktiles / n_ranges);
     const int kt1 = MASKED ? n_ktiles + 1 : (int)((int64_t)(range + 1) * n_ktiles / n_ranges);
-    const int ksteps = kc / 2;  // 64-column stages per key tile
+    const int T = (kt1 - kt0) * kc;  // 32-column stages of the whole range
 
+    // running best of each lane per 32-query fragment b: the score, and the 32-row group (global row / 32)
+    // holding it -- the exact row is recovered later by replaying that group (see launch.hpp)
     float best[QF];
-    int bidx[QF];
+    int bgrp[QF];
 #pragma unroll
     for (int q = 0; q < QF; ++q) {
         best[q] = -__builtin_inff();
-        bidx[q] = 0x7FFFFFFF;
+        bgrp[q] = 0x7FFFFFFF;
     }
 
-    f32x16 acc[4][QF];
-
-    // global -> LDS without registers: each wave copies whole 1 KiB chunks (lane l moves bytes 16l..16l+15)
-    // global -> LDS without registers: wave w copies chunks w, w+4, ..., lane l moving bytes 16l .. 16l+15
-    const uint32_t tile_bytes = (uint32_t)kTile * kc * 64;  // one 256-row tile of the tiled layout
+    // stage t = columns 32 (t % kc) .. 32 (t % kc) + 31 of key tile kt0 + t / kc, copied by buffer loads
+    // straight into LDS buffer t % kNBuf, kNBuf - 1 stages ahead.  Wave w copies chunks (16-row groups) w and
+    // w + 8 of both operands, lane l moving bytes 16 l .. 16 l + 15 of a chunk.
+    const uint32_t tile_bytes = (uint32_t)kTile * kc * 64;
     const __amdgpu_buffer_rsrc_t qr = make_rsrc(qt + (int64_t)qtile * 16 * kc * 64, tile_bytes);
     const uint32_t voff = (uint32_t)lane * 16;
-    auto load_stage = [&](int kt, int st, int buf) {
+    auto issue = [&](int t) {
+        const int kt = kt0 + t / kc, st = t % kc;
         const __amdgpu_buffer_rsrc_t kr = make_rsrc(keys + (int64_t)kt * 16 * kc * 64, tile_bytes);
-        unsigned char* dk = lds + buf * kStageBytes;
+        unsigned char* dk = lds + (t % kNBuf) * kStageBytes;
         unsigned char* dq = dk + kChunks * 1024;
 #pragma unroll
-        for (int p = 0; p < kChunks / kWaves; ++p) {
-            const int j = p * kWaves + wid;  // chunk 0..31 of the stage
-            const uint32_t soff = (uint32_t)(((j >> 1) * kc + st * 2 + (j & 1)) * 1024);
+        for (int p = 0; p < kPerWave; ++p) {
+            const int j = p * kWaves + wid;
+            const uint32_t soff = (uint32_t)((j * kc + st) * 1024);
             buffer_to_lds16(kr, voff, soff, dk + j * 1024);
             buffer_to_lds16(qr, voff, soff, dq + j * 1024);
         }
     };
 
-    // one flat loop over (key tile, 64-column stage); the next stage streams into the other buffer
-    const int T = (kt1 - kt0) * ksteps;
-    if (T > 0) load_stage(kt0, 0, 0);
-    wait_vm_all();
-    __syncthreads();
-#pragma unroll
-    for (int a = 0; a < 4; ++a)
-#pragma unroll
-        for (int b = 0; b < QF; ++b) acc[a][b] = f32x16{};
-
-    int kt = kt0, st = 0, buf = 0;
-    for (int t = 0; t < T; ++t) {
-        if (t + 1 < T) {
-            // buffer buf^1 was last read before the barrier that ended the previous stage
-            if (st + 1 < ksteps)
-                load_stage(kt, st + 1, buf ^ 1);
-            else
-                load_stage(kt + 1, 0, buf ^ 1);
-        }
-        const unsigned char* sk = lds + buf * kStageBytes;
+    f32x16 acc[4][QF];
+    int kt = kt0, st = 0;
+    // one stage: multiply LDS buffer t % kNBuf.  FIRST: the stage opens a key tile, so its first MFMAs
+    // start from a zero accumulator.
+    auto step = [&](int t, auto first_tag) {
+        constexpr bool FIRST = decltype(first_tag)::value;
+        // buffer (t + 3) % 4 was last read in stage t - 1, which ended with a barrier
+        if (t + kNBuf - 1 < T) issue(t + kNBuf - 1);
+        const unsigned char* sk = lds + (t % kNBuf) * kStageBytes;
         const unsigned char* sq = sk + kChunks * 1024;
-        // fragments of substep s+1 are read from LDS while the 16 MFMAs of substep s run
         u32x4 fa[2][4], fb[2][QF];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) fa[0][i] = *(const u32x4*)(sk + frag_offset(wk * 128 + i * 32, 0, lane));
+        for (int s = 0; s < 2; ++s) {
 #pragma unroll
-        for (int i = 0; i < QF; ++i) fb[0][i] = *(const u32x4*)(sq + frag_offset(wq * 32 * QF + i * 32, 0, lane));
+            for (int i = 0; i < 4; ++i) fa[s][i] = *(const u32x4*)(sk + frag_offset(wk * 128 + i * 32, s, lane));
 #pragma unroll
-        for (int s = 0; s < 4; ++s) {
-            const int cur = s & 1;
-            if (s < 3) {
+            for (int i = 0; i < QF; ++i) fb[s][i] = *(const u32x4*)(sq + frag_offset(wq * 64 + i * 32, s, lane));
+        }
 #pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    fa[cur ^ 1][i] = *(const u32x4*)(sk + frag_offset(wk * 128 + i * 32, s + 1, lane));
-#pragma unroll
-                for (int i = 0; i < QF; ++i)
-                    fb[cur ^ 1][i] = *(const u32x4*)(sq + frag_offset(wq * 32 * QF + i * 32, s + 1, lane));
-            }
+        for (int s = 0; s < 2; ++s)
 #pragma unroll
             for (int a = 0; a < 4; ++a)
 #pragma unroll
-                for (int b = 0; b < QF; ++b) acc[a][b] = mfma32x32x16(fa[cur][a], fb[cur][b], acc[a][b]);
-            __builtin_amdgcn_sched_barrier(0);
-        }
-        wait_vm_all();
-        __syncthreads();
-        buf ^= 1;
+                for (int b = 0; b < QF; ++b)
+                    acc[a][b] = mfma32x32x16(fa[s][a], fb[s][b], (FIRST && s == 0) ? f32x16{} : acc[a][b]);
 
-        if (++st == ksteps) {
-            // epilogue of key tile kt: lane holds, for query column wq*64 + b*32 + lane%32, the keys
-            // kt*256 + wk*128 + a*32 + 8*(r/4) + 4*(lane/32) + r%4, a = 0..3, r = 0..15 (increasing in (a, r))
-            const int rowbase = kt * kTile + wk * 128 + 4 * (lane >> 5);
-            const int valid = n_rows - rowbase;  // row rowbase + off is a stored entry iff off < valid
+        if (++st == kc) {
+            // end of key tile kt: lane holds, for query column wq*64 + b*32 + lane%32, the keys
+            // kt*256 + wk*128 + a*32 + 8*(r/4) + 4*(lane/32) + r%4 (a = 0..3, r = 0..15).  Per 32-row group a
+            // take the maximum; the first group reaching the overall maximum is the lowest-index candidate.
+            const int grp0 = (kt * kTile + wk * 128) >> 5;
+            const int valid = n_rows - (kt * kTile + wk * 128 + 4 * (lane >> 5));
 #pragma unroll
             for (int b = 0; b < QF; ++b) {
-                float m = -__builtin_inff();
+                float ma[4];
 #pragma unroll
-                for (int a = 0; a < 4; ++a)
+                for (int a = 0; a < 4; ++a) {
+                    float m = -__builtin_inff();
 #pragma unroll
                     for (int r = 0; r < 16; ++r) {
                         const int off = a * 32 + 8 * (r >> 2) + (r & 3);
                         m = fmaxf(m, (!MASKED || off < valid) ? acc[a][b][r] : -__builtin_inff());
                     }
-                const bool up = m > best[b];
-                if (__ballot(up) != 0ull) {
-                    int found = 0;
-#pragma unroll
-                    for (int a = 3; a >= 0; --a)
-#pragma unroll
-                        for (int r = 15; r >= 0; --r) {
-                            const int off = a * 32 + 8 * (r >> 2) + (r & 3);
-                            if ((!MASKED || off < valid) && acc[a][b][r] == m) found = off;
-                        }
-                    if (up) {
-                        best[b] = m;
-                        bidx[b] = rowbase + found;
-                    }
+                    ma[a] = m;
                 }
-                __builtin_amdgcn_sched_barrier(0);
+                const float m = fmaxf(fmaxf(ma[0], ma[1]), fmaxf(ma[2], ma[3]));
+                const int ga = ma[0] == m ? 0 : ma[1] == m ? 1 : ma[2] == m ? 2 : 3;
+                if (m > best[b]) {
+                    best[b] = m;
+                    bgrp[b] = grp0 + ga;
+                }
             }
-#pragma unroll
-            for (int a = 0; a < 4; ++a)
-#pragma unroll
-                for (int b = 0; b < QF; ++b) acc[a][b] = f32x16{};
             st = 0;
             ++kt;
         }
+        // stage t + 1 must have landed (for every wave) before the next stage reads it
+        const int last_issued = (t + kNBuf - 1 < T) ? t + kNBuf - 1 : T - 1;
+        const int after = last_issued - (t + 1);
+        wait_stages_in_flight(after < 0 ? 0 : after);
+        __syncthreads();
+    };
+
+    for (int t = 0; t < kNBuf - 1 && t < T; ++t) issue(t);
+    wait_stages_in_flight((T < kNBuf - 1 ? T : kNBuf - 1) - 1);
+    __syncthreads();
+    for (int t = 0; t < T; ++t) {
+        if (st == 0)
+            step(t, std::true_type{});
+        else
+            step(t, std::false_type{});
     }
 
     // merge lanes l and l^32 (same query), then the two key-half waves, and write one candidate per query
-    uint64_t* red = (uint64_t*)lds;  // [2 key halves][256 queries]; the LDS stages are no longer read
+    uint64_t* red = (uint64_t*)lds;  // [2 key halves][256 queries]; the stage buffers are no longer read
 #pragma unroll
     for (int b = 0; b < QF; ++b) {
-        uint64_t p = (bidx[b] == 0x7FFFFFFF) ? 0ull : pack_top1(best[b], bidx[b]);
+        uint64_t p = (bgrp[b] == 0x7FFFFFFF) ? 0ull : pack_top1(best[b], bgrp[b]);
         p = umax64(p, (uint64_t)__shfl_xor((unsigned long long)p, 32, kWave));
-        if (lane < 32) red[wk * kTile + wq * 32 * QF + b * 32 + lane] = p;
+        if (lane < 32) red[wk * kTile + wq * 64 + b * 32 + lane] = p;
     }
     __syncthreads();
     if (tid < kTile) {
-        const int q = tid;  // 0..255
-        const uint64_t m = umax64(red[q], red[kTile + q]);
-        const int gq = qtile * kTile + q;
+        const uint64_t m = umax64(red[tid], red[kTile + tid]);
+        const int gq = qtile * kTile + tid;
         if (gq < B) part[(int64_t)gq * P + (MASKED ? slot : range)] = m;
     }
 }
@@ -215,17 +228,27 @@ __global__ __launch_bounds__(512, 1) void k_stage1_gemm(const u32x4* __restrict_
 hipError_t launch_stage1_gemm(const uint16_t* keys, const uint16_t* qt, int B, int n_rows, int d_pad, uint64_t* part,
                               int num_cu, int* P_out, hipStream_t s) {
     const int kc = d_pad / 32;
-    if (kc % 2 != 0 || n_rows <= 0 || B <= 0) return hipErrorInvalidValue;
+    if (n_rows <= 0 || B <= 0) return hipErrorInvalidValue;
     const int n_qtiles = (B + kTile - 1) / kTile;
-    const int n_full = n_rows / kTile;              // key tiles without padded rows
-    const bool tail = n_rows % kTile != 0;          // one more, partial, tile
+    const int n_full = n_rows / kTile;      // key tiles without padded rows
+    const bool tail = n_rows % kTile != 0;  // one more, partial, tile
     // enough workgroups to fill every CU a few times over, each with a run of key tiles
     int n_ranges = (4 * num_cu + n_qtiles - 1) / n_qtiles;
     if (n_ranges > n_full) n_ranges = n_full;
     if (n_ranges > kMaxPartials - 1) n_ranges = kMaxPartials - 1;
     const int P = n_ranges + (tail ? 1 : 0);
     *P_out = P;
-    const size_t lds = 2 * (size_t)kStageBytes;
+    // XCD placement: xq query groups x (8 / xq) key parts, when the tile counts divide evenly
+    static const int xq_env = [] {
+        const char* e = std::getenv("LACACHE_GEMM_XQ");
+        return e ? std::atoi(e) : 2;
+    }();
+    const int grid = n_qtiles * n_ranges;
+    int xq = 0;
+    if ((xq_env == 1 || xq_env == 2 || xq_env == 4 || xq_env == 8) && n_qtiles % xq_env == 0 &&
+        n_ranges % (8 / xq_env) == 0)
+        xq = xq_env;
+    const size_t lds = (size_t)kNBuf * kStageBytes;
     static bool attr = false;
     if (!attr) {
         (void)hipFuncSetAttribute((const void*)k_stage1_gemm<false>, hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -235,11 +258,11 @@ hipError_t launch_stage1_gemm(const uint16_t* keys, const uint16_t* qt, int B, i
         attr = true;
     }
     if (n_ranges > 0)
-        k_stage1_gemm<false><<<dim3(n_qtiles * n_ranges), dim3(kWaves * 64), lds, s>>>(
-            (const u32x4*)keys, (const u32x4*)qt, kc, n_rows, B, n_qtiles, n_full, n_ranges, 0, P, part);
+        k_stage1_gemm<false><<<dim3(grid), dim3(kWaves * 64), lds, s>>>(
+            (const u32x4*)keys, (const u32x4*)qt, kc, n_rows, B, n_qtiles, n_full, n_ranges, 0, P, xq, part);
     if (tail)
         k_stage1_gemm<true><<<dim3(n_qtiles), dim3(kWaves * 64), lds, s>>>(
-            (const u32x4*)keys, (const u32x4*)qt, kc, n_rows, B, n_qtiles, n_full, 1, P - 1, P, part);
+            (const u32x4*)keys, (const u32x4*)qt, kc, n_rows, B, n_qtiles, n_full, 1, P - 1, P, 0, part);
     return hipGetLastError();
 }
 

@@ -13,8 +13,37 @@
 
 namespace lacache {
 
+// Exact row of query b inside the 32-row group g that the GEMM path reported: replay the group against
+// the same 32-query fragment with the same MFMA sequence (v_mfma_f32_32x32x16_bf16 over the 16-column
+// steps in order, from a zero accumulator), which reproduces the GEMM's float32 scores bit for bit, and
+// take the lowest stored row whose score equals s.  Returns -1 if none does.
+__device__ int32_t replay_group(const u32x4* __restrict__ keys, const u32x4* __restrict__ qt, int kc, int b, int g,
+                                float s, int n_rows, int lane) {
+    const int kr = g * 32 + (lane & 31);       // key row this lane feeds (row operand)
+    const int qr = (b & ~31) + (lane & 31);    // query row of the fragment (column operand)
+    const u32x4* kp = keys + (int64_t)(kr >> 4) * kc * 64 + (kr & 15);
+    const u32x4* qp = qt + (int64_t)(qr >> 4) * kc * 64 + (qr & 15);
+    f32x16 acc = f32x16{};
+    for (int st = 0; st < 2 * kc; ++st) {
+        const int off = (st >> 1) * 64 + (((st & 1) << 1) + (lane >> 5)) * 16;
+        acc = mfma32x32x16(kp[off], qp[off], st == 0 ? f32x16{} : acc);
+    }
+    int row = 0x7FFFFFFF;
+    if ((lane & 31) == (b & 31)) {
+#pragma unroll
+        for (int j = 15; j >= 0; --j) {
+            const int r = g * 32 + 8 * (j >> 2) + 4 * (lane >> 5) + (j & 3);
+            if (acc[j] == s && r < n_rows) row = r;
+        }
+    }
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) row = min(row, __shfl_xor(row, m, kWave));
+    return row == 0x7FFFFFFF ? -1 : row;
+}
+
 __global__ __launch_bounds__(256) void k_finalize_verify(
-    const uint64_t* __restrict__ part, int P, int B, int n_rows, const void* __restrict__ la, int dtype, int d,
+    const uint64_t* __restrict__ part, int P, int part_groups, const u32x4* __restrict__ keys_tiled,
+    const u32x4* __restrict__ qt, int kc, int B, int n_rows, const void* __restrict__ la, int dtype, int d,
     const int32_t* __restrict__ la_tok, int k, const uint16_t* __restrict__ emb, int d_pad,
     const int32_t* __restrict__ tokens, int k_cap, float tau_q, float tau_r, int32_t* __restrict__ idx_out,
     float* __restrict__ score_out, float* __restrict__ resp_out, int32_t* __restrict__ dec_out) {
@@ -34,8 +63,10 @@ __global__ __launch_bounds__(256) void k_finalize_verify(
     uint64_t m = 0;
     for (int p = lane; p < P; p += kWave) m = umax64(m, part[(int64_t)b * P + p]);
     m = wave_max_u64(m);
-    const int32_t i = unpack_idx(m);
-    const float score = fminf(fmaxf(unpack_score(m), -1.0f), 1.0f);
+    int32_t i = unpack_idx(m);
+    const float s_raw = unpack_score(m);
+    if (part_groups && m != 0ull) i = replay_group(keys_tiled, qt, kc, b, i, s_raw, n_rows, lane);
+    const float score = fminf(fmaxf(s_raw, -1.0f), 1.0f);
     // every stored row yields a candidate, so m != 0 here; the range check keeps the gathers in bounds regardless
     if (m == 0ull || i < 0 || i >= n_rows || !(score >= tau_q)) {
         if (lane == 0) {
@@ -96,14 +127,15 @@ __global__ __launch_bounds__(256) void k_finalize_verify(
     }
 }
 
-hipError_t launch_finalize_verify(const uint64_t* part, int P, int B, int n_rows, const void* la, int dtype, int d,
+hipError_t launch_finalize_verify(const uint64_t* part, int P, bool part_groups, const uint16_t* keys_tiled,
+                                  const uint16_t* qt, int B, int n_rows, const void* la, int dtype, int d,
                                   const int32_t* la_tok, int k, const uint16_t* emb, int d_pad,
                                   const int32_t* tokens, int k_cap, float tau_q, float tau_r, int32_t* idx,
                                   float* score, float* resp_score, int32_t* decision, hipStream_t s) {
     if (B <= 0) return hipSuccess;
-    k_finalize_verify<<<dim3((B + 3) / 4), dim3(256), 0, s>>>(part, P, B, n_rows, la, dtype, d, la_tok, k, emb,
-                                                              d_pad, tokens, k_cap, tau_q, tau_r, idx, score,
-                                                              resp_score, decision);
+    k_finalize_verify<<<dim3((B + 3) / 4), dim3(256), 0, s>>>(
+        part, P, part_groups ? 1 : 0, (const u32x4*)keys_tiled, (const u32x4*)qt, d_pad / 32, B, n_rows, la, dtype,
+        d, la_tok, k, emb, d_pad, tokens, k_cap, tau_q, tau_r, idx, score, resp_score, decision);
     return hipGetLastError();
 }
 

@@ -190,8 +190,8 @@ static int lookup_chunk(lacache_t h, const char* queries, const char* la, const 
                         float tau_r, int k, int32_t* idx, float* score, float* resp, int32_t* dec, hipStream_t s) {
     const int n_rows = (int)h->size;
     int P = 0;
+    const bool small = B <= h->b_small;
     if (n_rows > 0) {
-        const bool small = B <= h->b_small;
         const int64_t rows_pad = small ? round_up(B, 16) : round_up(B, kRowTile);
         if (launch_normalise(queries, h->dtype, B, rows_pad, h->d, h->d_pad, h->qt, 0, true, s) != hipSuccess)
             return LACACHE_EHIP;
@@ -206,8 +206,8 @@ static int lookup_chunk(lacache_t h, const char* queries, const char* la, const 
         if (e != hipSuccess) return LACACHE_EHIP;
         if (h->profiling && hipEventRecord(e1, s) != hipSuccess) return LACACHE_EHIP;
     }
-    if (launch_finalize_verify(h->part, P, B, n_rows, la, h->dtype, h->d, la_tok, k, h->emb, h->d_pad, h->tokens,
-                               h->k_cap, tau_q, tau_r, idx, score, resp, dec, s) != hipSuccess)
+    if (launch_finalize_verify(h->part, P, !small, h->keys, h->qt, B, n_rows, la, h->dtype, h->d, la_tok, k, h->emb,
+                               h->d_pad, h->tokens, h->k_cap, tau_q, tau_r, idx, score, resp, dec, s) != hipSuccess)
         return LACACHE_EHIP;
     return LACACHE_OK;
 }

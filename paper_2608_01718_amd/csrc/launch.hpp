@@ -24,13 +24,17 @@ hipError_t launch_export(const uint16_t* src, int64_t first, int n, int d, int d
 hipError_t launch_stage1_stream(const uint16_t* keys, const uint16_t* qt, int B, int n_rows, int d_pad,
                                 uint64_t* part, int num_cu, int* P_out, hipStream_t s);
 
-// Stage 1, compute-bound path (matrix-core GEMM with a fused row argmax):
-// queries qt (tiled, rows padded to a multiple of 256) against n_rows keys.
+// Stage 1, compute-bound path (matrix-core GEMM with a fused row maximum):
+// queries qt (tiled, rows padded to a multiple of 256) against n_rows keys.  Its partials name the
+// 32-row group of the candidate (global row / 32) instead of the row; the finalize step recovers the
+// row by replaying that group (part_groups = true).
 hipError_t launch_stage1_gemm(const uint16_t* keys, const uint16_t* qt, int B, int n_rows, int d_pad,
                               uint64_t* part, int num_cu, int* P_out, hipStream_t s);
 
-// Merge the P partial candidates of each query, threshold, and run stage 2 on hits.
-hipError_t launch_finalize_verify(const uint64_t* part, int P, int B, int n_rows, const void* la,
+// Merge the P partial candidates of each query (rows, or 32-row groups to replay against keys_tiled and
+// the tiled queries qt), threshold, and run stage 2 on hits.
+hipError_t launch_finalize_verify(const uint64_t* part, int P, bool part_groups, const uint16_t* keys_tiled,
+                                  const uint16_t* qt, int B, int n_rows, const void* la,
                                   int dtype, int d, const int32_t* la_tok, int k, const uint16_t* emb, int d_pad,
                                   const int32_t* tokens, int k_cap, float tau_q, float tau_r, int32_t* idx,
                                   float* score, float* resp_score, int32_t* decision, hipStream_t s);
