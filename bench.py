@@ -42,7 +42,73 @@ def parse():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="per-launch HBM traffic measured with rocprofv3 counters (JSON), if present")
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
+                    help="run one plain device copy of this many MiB (a known-size reference for the HBM "
+                         "counters) and exit")
+    ap.add_argument("--pmc-summary", default=None,
+                    help="directory holding rocprofv3 --pmc runs fetch_bench/, write_bench/, fetch_copy/, "
+                         "write_copy/: write the per-launch traffic of the stage-1 kernels to --traffic and exit")
+    ap.add_argument("--copy-mib", type=int, default=1024, help="size of the copy used by --pmc-summary")
     return ap.parse_args()
+
+
+STAGE1_KERNELS = {"serve_large": "k_stage1_gemm<false>", "serve_small": "k_stage1_stream<1>"}
+STAGE1_SOURCES = {"serve_large": ["k_stage1_gemm.hip", "common.hpp"],
+                  "serve_small": ["k_stage1_stream.hip", "common.hpp"]}
+
+
+def sources_digest(name):
+    """Digest of the sources of a workload's stage-1 kernel: counters are valid only for that code."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in STAGE1_SOURCES[name]:
+        h.update(open(os.path.join(ROOT, "paper_2608_01718_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def calibrate_copy(mib):
+    """One plain elementwise pass over a known number of bytes (reads mib MiB, writes mib MiB)."""
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.int32, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    torch.neg(src, out=dst)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": n * 4}), flush=True)
+
+
+def pmc_summary(root, out_path, copy_mib):
+    """Per-launch HBM traffic of the stage-1 kernels from FETCH_SIZE / WRITE_SIZE (KiB per dispatch), each
+    scaled by what the same counter reads for a plain copy of known size."""
+    import csv
+    import glob
+
+    def per_kernel(sub, counter):
+        vals = {}
+        for f in glob.glob(os.path.join(root, sub, "**", "*counter_collection.csv"), recursive=True):
+            for r in csv.DictReader(open(f)):
+                if r["Counter_Name"] == counter:
+                    vals.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
+        return vals
+
+    copy_bytes = copy_mib * (1 << 20)
+    f_copy = max((v for k, vs in per_kernel("fetch_copy", "FETCH_SIZE").items() for v in vs), default=None)
+    w_copy = max((v for k, vs in per_kernel("write_copy", "WRITE_SIZE").items() for v in vs), default=None)
+    fk, wk = per_kernel("fetch_bench", "FETCH_SIZE"), per_kernel("write_bench", "WRITE_SIZE")
+    out = {"copy_bytes": copy_bytes, "copy_fetch_kib": f_copy, "copy_write_kib": w_copy,
+           "fetch_scale": copy_bytes / (f_copy * 1024), "write_scale": copy_bytes / (w_copy * 1024)}
+    for name, kern in STAGE1_KERNELS.items():
+        fv = [v for k, vs in fk.items() if kern in k for v in vs]
+        wv = [v for k, vs in wk.items() if kern in k for v in vs]
+        if not fv or not wv:
+            continue
+        fetch = sorted(fv)[len(fv) // 2] * 1024 * out["fetch_scale"]
+        write = sorted(wv)[len(wv) // 2] * 1024 * out["write_scale"]
+        out[name] = {"kernel": kern, "sources_digest": sources_digest(name), "fetch_bytes": fetch,
+                     "write_bytes": write, "traffic_bytes": fetch + write, "dispatches": len(fv)}
+    json.dump(out, open(out_path, "w"), indent=1)
+    print(json.dumps(out), flush=True)
 
 
 def log(*a):
@@ -114,7 +180,9 @@ def run_workload(name, steps, warmup, lc, torch, synth, traffic_db, want_cpu):
     else:
         roof = dict(bound="hbm", achieved=key_bytes / (k_avg * 1e-3) / 1e9, peak=PEAK_HBM_GBS, unit="GB/s")
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = traffic_db.get(name)
+    t = traffic_db.get(name)
+    # counters describe the code they were taken on: a changed kernel reports no traffic
+    roof["traffic"] = t["traffic_bytes"] if t and t.get("sources_digest") == sources_digest(name) else None
     roof["kernel_avg_ms"] = k_avg
     res = dict(workload=name, value=call_b / (ms * 1e-3), unit="lookups/s", ms_per_step=ms, B=call_b,
                roofline=roof, rates=rates, config=dict(workload=describe(sp, call_b), N=sp.N, d=sp.d, B=call_b,
@@ -135,7 +203,7 @@ def cpu_baseline(sp, w, call_b):
     eq = oracle.quantise(w.emb, sp.in_dtype)
     t_store = time.time() - t0
     threads = oracle.num_threads()
-    n = max(threads, 16)
+    n = min(sp.B, 512)  # about 10-30 s of work on a 16-thread host
     qq = oracle.quantise(w.queries[:n], sp.in_dtype)
     aq = oracle.quantise(w.la_emb[:n], sp.in_dtype)
     u = np.ascontiguousarray(w.la_tok[:n, :sp.k])
@@ -149,10 +217,16 @@ def cpu_baseline(sp, w, call_b):
 
 def main():
     args = parse()
+    if args.pmc_summary:
+        pmc_summary(args.pmc_summary, args.traffic, args.copy_mib)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: the lookup is built and measured on a single MI355X; "
               "sharding the cache over GPUs is a design note, not part of this build.", file=sys.stderr)
         sys.exit(2)
+    if args.calibrate_copy_mib:
+        calibrate_copy(args.calibrate_copy_mib)
+        return
     import torch
     import synth
     from paper_2608_01718_amd import build as b

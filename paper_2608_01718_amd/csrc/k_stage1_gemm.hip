@@ -9,20 +9,22 @@
 //
 // Tiling: a workgroup of 8 waves owns a tile of 256 queries and walks a
 // contiguous range of 256-key tiles.  Each key tile is consumed in stages of
-// 32 columns: a stage (16 KiB of keys + 16 KiB of queries, 1 KiB chunks of the
-// tiled store layout) is copied by buffer loads straight into one of four LDS
-// buffers, three stages ahead of the one being multiplied, so the copies have
-// three stage-times to arrive from L2 or HBM.  Waves are arranged 2 (key
-// halves of 128) x 4 (query quarters of 64); a wave multiplies its 128 x 64
-// block with v_mfma_f32_32x32x16_bf16, keys as the row operand, so a lane's 16
-// accumulators per fragment are 16 keys of one query.  After the last stage of
-// a key tile each lane reduces its 64 keys per query in registers and updates
-// a running (best score, index); the scan for the index runs only when some
-// lane of the wave improved.  Key rows are visited in increasing order and
-// only a strictly larger score replaces the best, so ties keep the lowest
-// index.  The one partial key tile (rows beyond the entry count are zero
-// padding and must not win) is handled by a separate, masked instantiation.
-// At the end each workgroup writes one packed candidate per query.
+// kBK columns of d: a stage (256 x kBK keys + 256 x kBK queries, 1 KiB chunks
+// of the tiled store layout) is copied by buffer loads straight into one of
+// kNBuf LDS buffers (no staging registers), kNBuf - 1 stages ahead of the one
+// being multiplied.  Waves are arranged 2 (key halves of 128) x 4 (query
+// quarters of 64), two per SIMD; a wave multiplies its 128 x 64 block with
+// v_mfma_f32_32x32x16_bf16, keys as the row operand, so a lane's 16
+// accumulators per fragment are 16 keys of one query.  The first MFMAs of a
+// key tile start from a zero accumulator.  After the last stage of a key tile
+// each lane takes, per query, the maximum of each of its four 32-row groups
+// and keeps a running (best score, 32-row group); only a strictly larger score
+// replaces the best and the lowest group wins within a tile, so ties keep the
+// lowest group.  The exact lowest row is recovered afterwards by replaying the
+// winning group (launch.hpp), which keeps this epilogue branch-free.  The one
+// partial key tile (rows beyond the entry count are zero padding and must not
+// win) is handled by a separate, masked instantiation.  At the end each
+// workgroup writes one packed candidate per query.
 #include <cstdlib>
 #include <type_traits>
 
@@ -36,17 +38,29 @@ namespace {
 constexpr int kTile = 256;                           // queries and keys per workgroup tile
 constexpr int kWaves = 8;                            // 2 key halves x 4 query quarters
 constexpr int QF = 2;                                // 32-query MFMA fragments per wave
-constexpr int kNBuf = 4;                             // LDS stage buffers (prefetch distance kNBuf - 1)
-constexpr int kChunks = 16;                          // 1 KiB chunks per operand per stage (256 rows x 32 cols)
+#ifndef LACACHE_GEMM_BK
+#define LACACHE_GEMM_BK 64
+#endif
+#ifndef LACACHE_GEMM_NBUF
+#define LACACHE_GEMM_NBUF 2
+#endif
+constexpr int kBK = LACACHE_GEMM_BK;                 // columns of d per LDS stage (32 or 64)
+constexpr int kNBuf = LACACHE_GEMM_NBUF;             // LDS stage buffers (prefetch distance kNBuf - 1)
+constexpr int kBlk = kBK / 32;                       // 32-column blocks of the tiled layout per stage
+constexpr int kSub = kBK / 16;                       // MFMA k-steps (16 columns) per stage
+constexpr int kChunks = 16 * kBlk;                   // 1 KiB chunks per operand per stage
 constexpr int kStageBytes = 2 * kChunks * 1024;      // keys + queries
 constexpr int kPerWave = kChunks / kWaves;           // chunks of each operand a wave copies per stage
+constexpr int kLoadsPerStage = 2 * kPerWave;         // buffer loads per wave per stage
+static_assert((kNBuf & (kNBuf - 1)) == 0 && kNBuf * kStageBytes <= 160 * 1024, "LDS stage ring");
 
 // byte offset, inside one operand's stage, of the 32x32x16 fragment read by lane l:
-// rows [row0, row0 + 32), columns 16 s .. 16 s + 15 of the 32-column stage
+// rows [row0, row0 + 32), columns 16 s .. 16 s + 15 of the stage (chunk j of a stage = 16-row group
+// j / kBlk, 32-column block j % kBlk)
 __device__ inline int frag_offset(int row0, int s, int lane) {
     const int g = (row0 >> 4) + ((lane & 31) >> 4);  // 16-row group inside the 256-row tile
-    const int c = (s << 1) + (lane >> 5);            // 8-column chunk inside the 32-column block
-    return (g * 64 + c * 16 + (lane & 15)) * 16;
+    const int c = ((s & 1) << 1) + (lane >> 5);      // 8-column chunk inside the 32-column block
+    return ((g * kBlk + (s >> 1)) * 64 + c * 16 + (lane & 15)) * 16;
 }
 
 // Buffer resource over `bytes` bytes at `base`: loads through it outside [0, bytes) return zeros
@@ -62,15 +76,24 @@ __device__ inline void buffer_to_lds16(__amdgpu_buffer_rsrc_t r, uint32_t voff, 
                                              soff, 0, 0);
 }
 
+// s_waitcnt with the vector-memory count N and the other counters left free (gfx9 encoding).
+template <int N>
+__device__ inline void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
 // Wait until at most `stages` stages of this wave's copies are still in flight.
 __device__ inline void wait_stages_in_flight(int stages) {
-    static_assert(2 * kPerWave == 4, "vmcnt immediates below assume 4 copies per wave per stage");
-    if (stages >= 2)
-        asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+    static_assert(kNBuf <= 4, "up to three stages in flight");
+    if (stages >= 3)
+        wait_vmcnt<3 * kLoadsPerStage>();
+    else if (stages == 2)
+        wait_vmcnt<2 * kLoadsPerStage>();
     else if (stages == 1)
-        asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+        wait_vmcnt<kLoadsPerStage>();
     else
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        wait_vmcnt<0>();
 }
 
 }  // namespace
@@ -105,7 +128,7 @@ __global__ __launch_bounds__(512, 1) void k_stage1_gemm(const u32x4* __restrict_
     }
     const int kt0 = MASKED ? n_ktiles : (int)((int64_t)range * n_ktiles / n_ranges);
     const int kt1 = MASKED ? n_ktiles + 1 : (int)((int64_t)(range + 1) * n_ktiles / n_ranges);
-    const int T = (kt1 - kt0) * kc;  // 32-column stages of the whole range
+    const int T = (kt1 - kt0) * (kc / kBlk);  // stages of the whole range
 
     // running best of each lane per 32-query fragment b: the score, and the 32-row group (global row / 32)
     // holding it -- the exact row is recovered later by replaying that group (see launch.hpp)
@@ -117,23 +140,29 @@ __global__ __launch_bounds__(512, 1) void k_stage1_gemm(const u32x4* __restrict_
         bgrp[q] = 0x7FFFFFFF;
     }
 
-    // stage t = columns 32 (t % kc) .. 32 (t % kc) + 31 of key tile kt0 + t / kc, copied by buffer loads
-    // straight into LDS buffer t % kNBuf, kNBuf - 1 stages ahead.  Wave w copies chunks (16-row groups) w and
-    // w + 8 of both operands, lane l moving bytes 16 l .. 16 l + 15 of a chunk.
+    // stages are consumed in order; stage t covers columns kBK (t % spt) .. of key tile kt0 + t / spt and is
+    // copied by buffer loads straight into LDS buffer t % kNBuf, kNBuf - 1 stages ahead.  Wave w copies
+    // chunks w, w + 8, ... of both operands, lane l moving bytes 16 l .. 16 l + 15 of a chunk.
+    const int spt = kc / kBlk;  // stages per key tile
     const uint32_t tile_bytes = (uint32_t)kTile * kc * 64;
     const __amdgpu_buffer_rsrc_t qr = make_rsrc(qt + (int64_t)qtile * 16 * kc * 64, tile_bytes);
     const uint32_t voff = (uint32_t)lane * 16;
-    auto issue = [&](int t) {
-        const int kt = kt0 + t / kc, st = t % kc;
-        const __amdgpu_buffer_rsrc_t kr = make_rsrc(keys + (int64_t)kt * 16 * kc * 64, tile_bytes);
-        unsigned char* dk = lds + (t % kNBuf) * kStageBytes;
+    int i_kt = kt0, i_st = 0, i_buf = 0;  // next stage to copy
+    auto issue = [&]() {
+        const __amdgpu_buffer_rsrc_t kr = make_rsrc(keys + (int64_t)i_kt * 16 * kc * 64, tile_bytes);
+        unsigned char* dk = lds + i_buf * kStageBytes;
         unsigned char* dq = dk + kChunks * 1024;
 #pragma unroll
         for (int p = 0; p < kPerWave; ++p) {
             const int j = p * kWaves + wid;
-            const uint32_t soff = (uint32_t)((j * kc + st) * 1024);
+            const uint32_t soff = (uint32_t)((((j / kBlk) * kc) + i_st * kBlk + (j % kBlk)) * 1024);
             buffer_to_lds16(kr, voff, soff, dk + j * 1024);
             buffer_to_lds16(qr, voff, soff, dq + j * 1024);
+        }
+        i_buf = (i_buf + 1) & (kNBuf - 1);
+        if (++i_st == spt) {
+            i_st = 0;
+            ++i_kt;
         }
     };
 
@@ -143,27 +172,27 @@ __global__ __launch_bounds__(512, 1) void k_stage1_gemm(const u32x4* __restrict_
     // start from a zero accumulator.
     auto step = [&](int t, auto first_tag) {
         constexpr bool FIRST = decltype(first_tag)::value;
-        // buffer (t + 3) % 4 was last read in stage t - 1, which ended with a barrier
-        if (t + kNBuf - 1 < T) issue(t + kNBuf - 1);
-        const unsigned char* sk = lds + (t % kNBuf) * kStageBytes;
+        // buffer (t + kNBuf - 1) % kNBuf was last read in stage t - 1, which ended with a barrier
+        if (t + kNBuf - 1 < T) issue();
+        const unsigned char* sk = lds + (t & (kNBuf - 1)) * kStageBytes;
         const unsigned char* sq = sk + kChunks * 1024;
-        u32x4 fa[2][4], fb[2][QF];
+        u32x4 fa[kSub][4], fb[kSub][QF];
 #pragma unroll
-        for (int s = 0; s < 2; ++s) {
+        for (int s = 0; s < kSub; ++s) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) fa[s][i] = *(const u32x4*)(sk + frag_offset(wk * 128 + i * 32, s, lane));
 #pragma unroll
             for (int i = 0; i < QF; ++i) fb[s][i] = *(const u32x4*)(sq + frag_offset(wq * 64 + i * 32, s, lane));
         }
 #pragma unroll
-        for (int s = 0; s < 2; ++s)
+        for (int s = 0; s < kSub; ++s)
 #pragma unroll
             for (int a = 0; a < 4; ++a)
 #pragma unroll
                 for (int b = 0; b < QF; ++b)
                     acc[a][b] = mfma32x32x16(fa[s][a], fb[s][b], (FIRST && s == 0) ? f32x16{} : acc[a][b]);
 
-        if (++st == kc) {
+        if (++st == spt) {
             // end of key tile kt: lane holds, for query column wq*64 + b*32 + lane%32, the keys
             // kt*256 + wk*128 + a*32 + 8*(r/4) + 4*(lane/32) + r%4 (a = 0..3, r = 0..15).  Per 32-row group a
             // take the maximum; the first group reaching the overall maximum is the lowest-index candidate.
@@ -199,7 +228,7 @@ __global__ __launch_bounds__(512, 1) void k_stage1_gemm(const u32x4* __restrict_
         __syncthreads();
     };
 
-    for (int t = 0; t < kNBuf - 1 && t < T; ++t) issue(t);
+    for (int t = 0; t < kNBuf - 1 && t < T; ++t) issue();
     wait_stages_in_flight((T < kNBuf - 1 ? T : kNBuf - 1) - 1);
     __syncthreads();
     for (int t = 0; t < T; ++t) {
