@@ -213,8 +213,12 @@ def _class_counts(sp: Spec, B: int):
 
 
 def queries(sp: Spec, keys: np.ndarray, emb: np.ndarray, tokens: np.ndarray, dup_pairs: np.ndarray,
-            B: int | None = None, N: int | None = None, stream_chunk: int = 0):
-    """Draw B queries with their lookahead inputs against the first N entries."""
+            B: int | None = None, N: int | None = None, stream_chunk: int = 0, recent=None, recent_frac=0.1):
+    """Draw B queries with their lookahead inputs against the first N entries.
+
+    recent = (lo, hi): a fraction recent_frac of the planted queries aims at rows lo .. hi-1 (the latest
+    insert batch of an interleaved insert/lookup schedule).
+    """
     B = sp.B if B is None else B
     N = keys.shape[0] if N is None else N
     d, k = sp.d, sp.k
@@ -232,6 +236,11 @@ def queries(sp: Spec, keys: np.ndarray, emb: np.ndarray, tokens: np.ndarray, dup
         # a random target that is the later copy of a duplicate pair is the earlier copy's key too
         later = dict(zip(dup_pairs[:, 1].tolist(), dup_pairs[:, 0].tolist()))
         target = np.array([later.get(int(t), int(t)) for t in target], np.int64)
+    if recent is not None and np_:
+        pl_idx = np.nonzero(planted)[0]
+        nr = int(round(recent_frac * np_))
+        sel = rng.choice(pl_idx, size=nr, replace=False)
+        target[sel] = rng.integers(recent[0], recent[1], nr)
     # benign queries aimed at exact-duplicate pairs: near key i (== key j), carrying j's lookahead
     nd = min(sp.n_dup_queries, nb, len(dup_pairs))
     dsel = rng.choice(len(dup_pairs), size=nd, replace=False) if nd else np.zeros(0, np.int64)

@@ -277,3 +277,44 @@ def test_errors_with_live_handle(lc):
     for j in range(4):
         assert torch.equal(whole[j].view(torch.int32), torch.cat([p[j] for p in parts]).view(torch.int32))
     c.close()
+
+
+def test_parity_large_full_size_interleaved(lc):
+    """The large clustered workload at full size: 4,000,000 x 1024 keys (top-2 margins often below 2e-3),
+    k = 32, 1024 queries per lookup, an insert batch of 4096 entries between lookups, 10% of the planted
+    queries aimed at the latest batch; sampled rows against the oracle after every step."""
+    import time
+    sp = synth.spec("large")
+    steps, batch = 3, 4096
+    total = sp.N + steps * batch
+    t0 = time.time()
+    keys, emb, tok = synth.entries(sp, 0, total)
+    say(f"[case] large full size: generated {total} entries in {time.time() - t0:.1f}s")
+    kq, eq, tq = oracle_store(sp, keys, emb, tok)
+    say(f"[case] large full size: oracle store quantised ({time.time() - t0:.1f}s)")
+    c = gpu_cache(lc, sp, keys[:sp.N], emb[:sp.N], tok[:sp.N], capacity=total, max_batch=sp.B,
+                  insert_chunk=1 << 18)
+    n = sp.N
+    for step in range(steps + 1):
+        recent = (n - batch, n) if step > 0 else None
+        q = synth.queries(sp, keys, emb, tok, np.zeros((0, 2), np.int64), B=sp.B, N=n, stream_chunk=100 + step,
+                          recent=recent)
+        g = gpu_lookup(c, q["queries"], q["la_emb"], q["la_tok"], sp.tau_q, sp.tau_r, sp.k)
+        rows = sample_rows(q["cls"], q["target"], 30, seed=step)
+        if recent is not None:
+            aimed = np.nonzero((q["target"] >= recent[0]) & (q["cls"] == synth.CLS_BENIGN))[0][:8]
+            rows = np.unique(np.concatenate([rows, aimed]))
+        qq, aq = oracle.quantise(q["queries"], sp.in_dtype), oracle.quantise(q["la_emb"], sp.in_dtype)
+        u = np.ascontiguousarray(q["la_tok"][:, :sp.k])
+        o = oracle.lookup(kq[:n], eq[:n], tq[:n], qq[rows], aq[rows], u[rows], sp.tau_q, sp.tau_r, sp.k)
+        stats = compare(g, o, kq[:n], eq[:n], tq[:n], qq, aq, u, sp.tau_q, sp.tau_r, sp.k, rows)
+        say(f"[ok] large step {step} N={n}: {stats} ({time.time() - t0:.1f}s)")
+        # the whole batch: planted benign queries are served, collisions rejected
+        ben, col = q["cls"] == synth.CLS_BENIGN, q["cls"] == synth.CLS_COLLISION
+        assert np.all(np.isin(g["decision"][ben], [oracle.HIT, oracle.HIT_EXACT]))
+        assert np.all(g["decision"][col] == oracle.REJECT)
+        if step < steps:
+            first = c.insert(to_dev(keys[n:n + batch]), to_dev(emb[n:n + batch]), to_dev(tok[n:n + batch]))
+            assert first == n
+            n += batch
+    c.close()
