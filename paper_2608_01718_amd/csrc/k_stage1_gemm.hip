@@ -191,6 +191,20 @@ __global__ __launch_bounds__(512, 1) void k_stage1_gemm(const u32x4* __restrict_
 #pragma unroll
                 for (int b = 0; b < QF; ++b)
                     acc[a][b] = mfma32x32x16(fa[s][a], fb[s][b], (FIRST && s == 0) ? f32x16{} : acc[a][b]);
+        // instruction order: the fragment reads of substep 0, then each substep's MFMAs interleaved one to
+        // one with the next substep's fragment reads, so LDS latency hides behind matrix-core work
+        constexpr int kReads = 4 + QF, kMfma = 4 * QF;
+        __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);  // DS reads
+#pragma unroll
+        for (int s = 1; s < kSub; ++s) {
+#pragma unroll
+            for (int i = 0; i < kReads; ++i) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
+            }
+            __builtin_amdgcn_sched_group_barrier(0x008, kMfma - kReads, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, kMfma, 0);
 
         if (++st == spt) {
             // end of key tile kt: lane holds, for query column wq*64 + b*32 + lane%32, the keys
