@@ -81,6 +81,50 @@ __device__ inline uint64_t wave_max_u64(uint64_t x) {
 }
 
 // ---------------------------------------------------------------------------
+// One wave L2-normalises one input row and rounds it to bfloat16: the sum of
+// squares is taken in double (lane-local in column order, then the butterfly
+// above), n = sqrt in double, and each component v / n is rounded once to
+// bfloat16.  A zero row (or live == false) gives zeros, as do the columns
+// d .. d_pad-1.  Lane l produces columns 8l + 512t .. 8l + 512t + 7 and hands
+// them, packed, to emit(j0, u32x4).  Every kernel that quantises a vector
+// (insert, query staging, lookahead check) goes through this routine, so equal
+// inputs quantise to identical bits wherever they are stored.
+// ---------------------------------------------------------------------------
+template <class Emit>
+__device__ inline void normalise_row(const void* row, int dtype, int d, int d_pad, bool live, int lane, Emit emit) {
+    double ss = 0.0;
+    if (live) {
+        for (int j0 = lane * 8; j0 < d; j0 += 512) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int j = j0 + e;
+                if (j < d) {
+                    const double v = load_in(row, dtype, j);
+                    ss += v * v;
+                }
+            }
+        }
+    }
+    ss = wave_sum_f64(ss);
+    const double n = __builtin_sqrt(ss);
+    for (int j0 = lane * 8; j0 < d_pad; j0 += 512) {
+        uint16_t h[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const int j = j0 + e;
+            h[e] = 0;
+            if (live && j < d && n != 0.0) h[e] = bf16_rne_from_f64(load_in(row, dtype, j) / n);
+        }
+        u32x4 w;
+        w.x = (uint32_t)h[0] | ((uint32_t)h[1] << 16);
+        w.y = (uint32_t)h[2] | ((uint32_t)h[3] << 16);
+        w.z = (uint32_t)h[4] | ((uint32_t)h[5] << 16);
+        w.w = (uint32_t)h[6] | ((uint32_t)h[7] << 16);
+        emit(j0, w);
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Top-1 candidates as one 64-bit key: high word = the score's bits mapped so
 // that unsigned order equals float order, low word = ~index.  The unsigned
 // maximum is then "highest score, lowest index among equal scores": a total

@@ -10,8 +10,7 @@
 
 namespace lacache {
 
-// One wave per row.  Rows >= rows (up to rows_pad) are written as zeros, as
-// are the columns d .. d_pad-1.  Lane l owns columns 8l + 512t .. 8l + 512t + 7.
+// One wave per row.  Rows >= rows (up to rows_pad) are written as zeros, as are the columns d .. d_pad-1.
 template <bool TILED>
 __global__ __launch_bounds__(256) void k_normalise_rows(const void* __restrict__ in, int dtype, int64_t rows,
                                                         int64_t rows_pad, int d, int d_pad,
@@ -21,39 +20,11 @@ __global__ __launch_bounds__(256) void k_normalise_rows(const void* __restrict__
     if (r >= rows_pad) return;
     const bool live = r < rows;
     const char* src = (const char*)in + (live ? r * (int64_t)d * (dtype == 0 ? 4 : 2) : 0);
-
-    double ss = 0.0;
-    if (live) {
-        for (int j0 = lane * 8; j0 < d; j0 += 512) {
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const int j = j0 + e;
-                if (j < d) {
-                    const double v = load_in(src, dtype, j);
-                    ss += v * v;
-                }
-            }
-        }
-    }
-    ss = wave_sum_f64(ss);
-    const double n = __builtin_sqrt(ss);
     const int kc = d_pad >> 5;
-    for (int j0 = lane * 8; j0 < d_pad; j0 += 512) {
-        uint16_t h[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            const int j = j0 + e;
-            h[e] = 0;
-            if (live && j < d && n != 0.0) h[e] = bf16_rne_from_f64(load_in(src, dtype, j) / n);
-        }
-        u32x4 w;
-        w.x = (uint32_t)h[0] | ((uint32_t)h[1] << 16);
-        w.y = (uint32_t)h[2] | ((uint32_t)h[3] << 16);
-        w.z = (uint32_t)h[4] | ((uint32_t)h[5] << 16);
-        w.w = (uint32_t)h[6] | ((uint32_t)h[7] << 16);
+    normalise_row(src, dtype, d, d_pad, live, lane, [&](int j0, u32x4 w) {
         const int64_t off = TILED ? tiled_offset(row0 + r, j0, kc) : (row0 + r) * (int64_t)d_pad + j0;
         *(u32x4*)(out + off) = w;
-    }
+    });
 }
 
 // Copy rows first .. first+n-1 of a bfloat16 matrix (tiled or row-major with

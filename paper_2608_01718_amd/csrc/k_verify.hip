@@ -80,33 +80,18 @@ __global__ __launch_bounds__(256) void k_finalize_verify(
 
     // normalise the lookahead embedding exactly as stored vectors are, and dot it with the entry's prefix row
     const char* src = (const char*)la + (int64_t)b * d * (dtype == 0 ? 4 : 2);
-    double ss = 0.0;
-    for (int j0 = lane * 8; j0 < d; j0 += 512) {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            const int j = j0 + e;
-            if (j < d) {
-                const double v = load_in(src, dtype, j);
-                ss += v * v;
-            }
-        }
-    }
-    ss = wave_sum_f64(ss);
-    const double n = __builtin_sqrt(ss);
-    const uint16_t* er = emb + (int64_t)i * d_pad;
+    const u32x4* er = (const u32x4*)(emb + (int64_t)i * d_pad);
     float acc = 0.0f;
-    if (n != 0.0) {
-        for (int j0 = lane * 8; j0 < d; j0 += 512) {
+    normalise_row(src, dtype, d, d_pad, true, lane, [&](int j0, u32x4 w) {
+        const u32x4 e = er[j0 >> 3];
+        const uint32_t av[4] = {w.x, w.y, w.z, w.w}, ev[4] = {e.x, e.y, e.z, e.w};
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const int j = j0 + e;
-                if (j < d) {
-                    const float a = bf16_to_f32(bf16_rne_from_f64(load_in(src, dtype, j) / n));
-                    acc += a * bf16_to_f32(er[j]);  // bf16 x bf16 is exact in float
-                }
-            }
+        for (int t = 0; t < 4; ++t) {
+            // bf16 x bf16 products are exact in float; padded columns are zero on both sides
+            acc += __uint_as_float(av[t] << 16) * __uint_as_float(ev[t] << 16);
+            acc += __uint_as_float(av[t] & 0xFFFF0000u) * __uint_as_float(ev[t] & 0xFFFF0000u);
         }
-    }
+    });
     acc = wave_sum_f32(acc);
     const float r = fminf(fmaxf(acc, -1.0f), 1.0f);
 
