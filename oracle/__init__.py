@@ -23,7 +23,8 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 SRC = os.path.join(_HERE, "lacache_oracle.c")
-LIB = os.path.join(_HERE, "liblacache_oracle.so")
+# LACACHE_ORACLE_LIB points the wrapper at another build of the same source (the mutation tests use it)
+LIB = os.environ.get("LACACHE_ORACLE_LIB", os.path.join(_HERE, "liblacache_oracle.so"))
 
 MISS, REJECT, HIT, HIT_EXACT = 0, 1, 2, 3
 F32, BF16 = 0, 1

@@ -1,0 +1,57 @@
+"""The pins are strong enough: each plausible mistake planted in a copy of the oracle's C source (a dropped
+term, a wrong sign, a flipped comparison, a transposed operand, a wrong rounding rule...) makes
+test_oracle_pins.py fail, while the unmodified source passes the same pipeline."""
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "lacache_oracle.c")
+
+MUTANTS = {
+    "ties go to the highest index": ("if (s > best) {", "if (s >= best) {"),
+    "dot product drops its last term": ("for (int32_t j = 0; j < d; ++j)\n        s += widen_bf16",
+                                        "for (int32_t j = 0; j < d - 1; ++j)\n        s += widen_bf16"),
+    "dot product subtracts": ("s += widen_bf16(x[j]) * widen_bf16(y[j]);", "s -= widen_bf16(x[j]) * widen_bf16(y[j]);"),
+    "stage 2 reads the key instead of the prefix embedding": ("lco_dot(a, emb + i * (int64_t)d, d)",
+                                                              "lco_dot(a, keys + i * (int64_t)d, d)"),
+    "stage-1 threshold is strict": ("if (!(score >= tau_q))", "if (!(score > tau_q))"),
+    "stage-2 threshold is strict": ("return (r >= tau_r) ? LCO_HIT : LCO_REJECT;",
+                                    "return (r > tau_r) ? LCO_HIT : LCO_REJECT;"),
+    "rounding ties go up": ("double r = nearbyint(ldexp(v, 7 - lead));", "double r = floor(ldexp(v, 7 - lead) + 0.5);"),
+    "norm without square root": ("double n = sqrt(ss);", "double n = ss;"),
+    "token compare skips the last token": ("for (int32_t j = 0; j < k; ++j)\n        if (u[j]",
+                                           "for (int32_t j = 0; j < k - 1; ++j)\n        if (u[j]"),
+    "no clamp at 1": ("    if (f > 1.0f)\n        f = 1.0f;\n", ""),
+    "identical tokens also need the embedding": ("    if (tok_eq)\n        return LCO_HIT_EXACT;",
+                                                 "    if (tok_eq && r >= tau_r)\n        return LCO_HIT_EXACT;"),
+    "second-best never updated": ("} else if (s > second) {", "} else if (s > best) {"),
+    "subnormal grid not clamped": ("if (lead < -126)\n        lead = -126;", ""),
+}
+
+
+def _run_pins(tmp_path, source: str, tag: str) -> int:
+    c = tmp_path / f"{tag}.c"
+    so = tmp_path / f"{tag}.so"
+    c.write_text(source)
+    subprocess.run(["gcc", "-O2", "-fopenmp", "-std=c11", "-shared", "-fPIC", "-o", str(so), str(c), "-lm"],
+                   check=True)
+    env = dict(os.environ, LACACHE_ORACLE_LIB=str(so))
+    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
+                        os.path.join(ROOT, "tests", "test_oracle_pins.py")], cwd=ROOT, env=env,
+                       capture_output=True, text=True)
+    return r.returncode
+
+
+def test_unmodified_source_passes_the_pins(tmp_path):
+    assert _run_pins(tmp_path, open(SRC).read(), "original") == 0
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_planted_mistake_is_caught(tmp_path, name):
+    old, new = MUTANTS[name]
+    src = open(SRC).read()
+    assert src.count(old) == 1, f"mutation anchor not found (or ambiguous): {name}"
+    assert _run_pins(tmp_path, src.replace(old, new), "mutant") != 0, f"pins did not catch: {name}"
