@@ -60,6 +60,7 @@ def lib():
         L.lco_first_identical.argtypes = [P, i64, i32, i64]
         L.lco_first_identical.restype = i64
         L.lco_num_threads.restype = ctypes.c_int
+        L.lco_lookup_ensemble.argtypes = [P, i64, i32, P, i32, f32, i32, P, P, P, P, P, i32, P, i32, P, P, P, P]
         _lib = L
     return _lib
 
@@ -144,6 +145,36 @@ def decide(keys_q, emb_q, tokens, q_q, a_q, u, tau_q: float, tau_r: float, k: in
     lib().lco_decide(_ptr(keys_q), _ptr(emb_q), _ptr(tokens), N, d, k_cap, _ptr(q_q), _ptr(a_q), _ptr(u), B,
                      tau_q, tau_r, k, _ptr(at), _ptr(out["s"]), _ptr(out["score"]), _ptr(out["resp_score"]),
                      _ptr(out["decision"]))
+    return out
+
+
+def lookup_ensemble(keys_q, q_q, tau_q: float, embs_q, as_q, tau_r, tokens, u, k: int) -> dict:
+    """Two-stage lookup with m lookahead models: embs_q[i] is [N][d_i], as_q[i] is [B][d_i], tau_r[i] a float.
+
+    Returns idx, score, resp_score ([B][m]), decision."""
+    keys_q = _c(keys_q, np.uint16)
+    N, d = keys_q.shape
+    q_q = _c(q_q, np.uint16).reshape(-1, d)
+    B = q_q.shape[0]
+    m = len(embs_q)
+    assert len(as_q) == m and len(tau_r) == m and m >= 1
+    embs = [_c(e, np.uint16) for e in embs_q]
+    las = [_c(a, np.uint16).reshape(B, -1) for a in as_q]
+    dm = np.array([e.shape[1] for e in embs], np.int32)
+    for e, a in zip(embs, las):
+        assert e.shape[0] == N and a.shape[1] == e.shape[1]
+    tokens = _c(tokens, np.int32)
+    u = _c(u, np.int32).reshape(B, -1)
+    assert u.shape[1] == k and 1 <= k <= tokens.shape[1]
+    emb_ptrs = (ctypes.c_void_p * m)(*[e.ctypes.data for e in embs])
+    la_ptrs = (ctypes.c_void_p * m)(*[a.ctypes.data for a in las])
+    tr = np.ascontiguousarray(tau_r, np.float32)
+    out = dict(idx=np.empty(B, np.int32), score=np.empty(B, np.float32), resp_score=np.empty((B, m), np.float32),
+               decision=np.empty(B, np.int32))
+    lib().lco_lookup_ensemble(_ptr(keys_q), N, d, _ptr(q_q), B, tau_q, m, ctypes.cast(emb_ptrs, ctypes.c_void_p),
+                              _ptr(dm), ctypes.cast(la_ptrs, ctypes.c_void_p), _ptr(tr), _ptr(tokens),
+                              tokens.shape[1], _ptr(u), k, _ptr(out["idx"]), _ptr(out["score"]),
+                              _ptr(out["resp_score"]), _ptr(out["decision"]))
     return out
 
 

@@ -168,6 +168,32 @@ static int32_t decide_one(const uint16_t *keys, const uint16_t *emb, const int32
 }
 
 /*
+ * Stage 1 (Algorithm 1, search with the query key): the entry of highest
+ * similarity, scanning entries in index order and replacing the best only on a
+ * strictly larger score, so the lowest index wins exact ties.  *second
+ * receives the best score over every other entry (-inf when N == 1).
+ */
+static int64_t top1(const uint16_t *keys, int64_t N, int32_t d, const uint16_t *qb, double *best_out,
+                    double *second_out)
+{
+    double best = -INFINITY, second = -INFINITY;
+    int64_t bi = -1;
+    for (int64_t i = 0; i < N; ++i) {
+        double s = lco_dot(qb, keys + i * (int64_t)d, d);
+        if (s > best) {
+            second = best;
+            best = s;
+            bi = i;
+        } else if (s > second) {
+            second = s;
+        }
+    }
+    *best_out = best;
+    *second_out = second;
+    return bi;
+}
+
+/*
  * The full two-stage lookup over quantised inputs.
  *   keys, emb : [N][d]     quantised cache keys and response-prefix embeddings
  *   tokens    : [N][k_cap] stored response-prefix token IDs
@@ -195,18 +221,8 @@ void lco_lookup(const uint16_t *keys, const uint16_t *emb, const int32_t *tokens
             margin[b] = (double)quiet_nan();
             continue;
         }
-        double best = -INFINITY, second = -INFINITY;
-        int64_t bi = -1;
-        for (int64_t i = 0; i < N; ++i) {
-            double s = lco_dot(qb, keys + i * (int64_t)d, d);
-            if (s > best) {
-                second = best;
-                best = s;
-                bi = i;
-            } else if (s > second) {
-                second = s;
-            }
-        }
+        double best, second;
+        int64_t bi = top1(keys, N, d, qb, &best, &second);
         idx[b] = (int32_t)bi;
         margin[b] = best - second;
         double s;
@@ -268,4 +284,51 @@ int lco_num_threads(void)
         n = omp_get_num_threads();
     }
     return n;
+}
+
+/*
+ * The lookup with an ensemble of m lookahead checks (Section 4.4: m independent
+ * indexing functions h_1..h_m; a cache hit is valid only if the key check
+ * passes and every h_i(f_k(x)) agrees with h_i(f_k(x'))).  Each entry stores
+ * one response-prefix embedding per model i (emb[i], [N][d_i]); each query
+ * brings its lookahead embedding under every model (a[i], [B][d_i]) and there
+ * is one threshold tau_r[i] per model.  Stage 1 is the same top-1 as
+ * lco_lookup.  Stage 2 (on a stage-1 hit only) passes when the first k tokens
+ * are identical, or when the cosine under every model reaches its threshold.
+ * resp_score is [B][m] (NaN where stage 2 did not run).
+ */
+void lco_lookup_ensemble(const uint16_t *keys, int64_t N, int32_t d, const uint16_t *q, int32_t B, float tau_q,
+                         int32_t m, const uint16_t *const *emb, const int32_t *d_m, const uint16_t *const *a,
+                         const float *tau_r, const int32_t *tokens, int32_t k_cap, const int32_t *u, int32_t k,
+                         int32_t *idx, float *score, float *resp_score, int32_t *decision)
+{
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int32_t b = 0; b < B; ++b) {
+        for (int32_t i = 0; i < m; ++i)
+            resp_score[(int64_t)b * m + i] = quiet_nan();
+        decision[b] = LCO_MISS;
+        if (N == 0) {
+            idx[b] = -1;
+            score[b] = quiet_nan();
+            continue;
+        }
+        double best, second;
+        int64_t bi = top1(keys, N, d, q + (int64_t)b * d, &best, &second);
+        idx[b] = (int32_t)bi;
+        score[b] = clamp_unit(best);
+        if (!(score[b] >= tau_q))
+            continue;
+        int all_pass = 1;
+        for (int32_t i = 0; i < m; ++i) {
+            float r = clamp_unit(lco_dot(a[i] + (int64_t)b * d_m[i], emb[i] + bi * (int64_t)d_m[i], d_m[i]));
+            resp_score[(int64_t)b * m + i] = r;
+            if (!(r >= tau_r[i]))
+                all_pass = 0;
+        }
+        int tok_eq = 1;
+        for (int32_t j = 0; j < k; ++j)
+            if (u[(int64_t)b * k + j] != tokens[bi * (int64_t)k_cap + j])
+                tok_eq = 0;
+        decision[b] = tok_eq ? LCO_HIT_EXACT : (all_pass ? LCO_HIT : LCO_REJECT);
+    }
 }

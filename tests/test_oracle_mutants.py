@@ -29,6 +29,11 @@ MUTANTS = {
                                                  "    if (tok_eq && r >= tau_r)\n        return LCO_HIT_EXACT;"),
     "second-best never updated": ("} else if (s > second) {", "} else if (s > best) {"),
     "subnormal grid not clamped": ("if (lead < -126)\n        lead = -126;", ""),
+    "ensemble checks only the first model": ("if (!(r >= tau_r[i]))", "if (i == 0 && !(r >= tau_r[i]))"),
+    "ensemble applies the first threshold to every model": ("if (!(r >= tau_r[i]))", "if (!(r >= tau_r[0]))"),
+    "ensemble needs the embeddings even for identical tokens": (
+        "decision[b] = tok_eq ? LCO_HIT_EXACT : (all_pass ? LCO_HIT : LCO_REJECT);",
+        "decision[b] = all_pass ? (tok_eq ? LCO_HIT_EXACT : LCO_HIT) : LCO_REJECT;"),
 }
 
 

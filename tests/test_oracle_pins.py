@@ -401,3 +401,92 @@ def test_paper_thresholds_fixture():
     assert sp.k == g["k"] and sp.d == g["embedding_dim"]["BGE"]
     for name, row in g["tau_a"].items():
         assert abs(min(row["cap"], row["P10"]) - row["used"]) < 1e-9, name
+
+
+# --------------------------------------------------------------------------- ensemble of lookahead checks
+
+
+def _ensemble_case(rng, N, d, dms, B, k_cap):
+    keys = oracle.quantise(rng.standard_normal((N, d)).astype(np.float32), oracle.F32)
+    embs = [oracle.quantise(rng.standard_normal((N, dm)).astype(np.float32), oracle.F32) for dm in dms]
+    tokens = rng.integers(0, 20, (N, k_cap), dtype=np.int32)
+    q = oracle.quantise(rng.standard_normal((B, d)).astype(np.float32), oracle.F32)
+    pick = rng.integers(0, N, B)
+    q[: B // 2] = keys[pick[: B // 2]]
+    las = []
+    for e, dm in zip(embs, dms):
+        a = rng.standard_normal((B, dm)).astype(np.float32)
+        # some lookaheads close to the candidate's prefix under this model, some far
+        # noise scales spread the prefix cosines of the close ones over roughly 0.45 .. 0.98
+        scale = rng.uniform(0.2, 2.0, (B // 3, 1)).astype(np.float32)
+        a[: B // 3] = bf.widen(e[pick[: B // 3]]) + scale * rng.standard_normal((B // 3, dm)).astype(np.float32) \
+            / np.sqrt(dm)
+        las.append(oracle.quantise(a, oracle.F32))
+    u = rng.integers(0, 20, (B, k_cap), dtype=np.int32)
+    u[: B // 6] = tokens[pick[: B // 6]]
+    return keys, embs, tokens, q, las, u
+
+
+def test_ensemble_of_one_is_the_plain_lookup():
+    rng = np.random.default_rng(31)
+    keys, embs, tokens, q, las, u = _ensemble_case(rng, 400, 48, [48], 60, 6)
+    for tq, tr in [(0.5, 0.6), (-1.0, -1.0), (0.9, 0.99)]:
+        e = oracle.lookup_ensemble(keys, q, tq, embs, las, [tr], tokens, u, 6)
+        o = oracle.lookup(keys, embs[0], tokens, q, las[0], u, tq, tr, 6)
+        np.testing.assert_array_equal(e["idx"], o["idx"])
+        np.testing.assert_array_equal(e["score"], o["score"])
+        np.testing.assert_array_equal(e["decision"], o["decision"])
+        np.testing.assert_array_equal(e["resp_score"][:, 0], o["resp_score"])
+
+
+def test_ensemble_matches_bruteforce_and_rule():
+    """Section 4.4: the lookahead passes only if every one of the m checks passes (identical tokens pass all)."""
+    rng = np.random.default_rng(32)
+    dms = [32, 48, 64]
+    keys, embs, tokens, q, las, u = _ensemble_case(rng, 500, 40, dms, 90, 5)
+    S = bf.scores(q, keys)
+    idx = np.argmax(S, axis=1)
+    score = np.clip(S[np.arange(90), idx].astype(np.float32), -1, 1)
+    hit = score >= np.float32(0.5)
+    R = np.stack([np.clip(np.einsum("bd,bd->b", bf.widen(a), bf.widen(em[idx])).astype(np.float32), -1, 1)
+                  for a, em in zip(las, embs)], axis=1)
+    tok_eq = np.all(u == tokens[idx], axis=1)
+    # fixed thresholds, then per-model thresholds at different quantiles of that model's own prefix scores,
+    # so that applying one model's threshold to another changes decisions
+    close = R[hit & (R.min(axis=1) > 0.2)]
+    assert len(close) >= 10
+    quant = [float(np.quantile(close[:, i], qv)) for i, qv in enumerate((0.1, 0.4, 0.25))]
+    for taus in ([0.3, 0.5, 0.4], quant, quant[::-1]):
+        e = oracle.lookup_ensemble(keys, q, 0.5, embs, las, taus, tokens, u, 5)
+        np.testing.assert_array_equal(e["idx"], idx)
+        all_pass = np.all(R >= np.array(taus, np.float32)[None, :], axis=1)
+        want = np.where(~hit, oracle.MISS, np.where(tok_eq, oracle.HIT_EXACT,
+                                                   np.where(all_pass, oracle.HIT, oracle.REJECT)))
+        np.testing.assert_array_equal(e["decision"], want)
+        np.testing.assert_array_equal(e["resp_score"][hit], R[hit])
+        assert np.all(np.isnan(e["resp_score"][~hit]))
+        assert (e["decision"] == oracle.HIT).sum() > 3 and (e["decision"] == oracle.REJECT).sum() > 3
+
+
+def test_ensemble_monotone_and_order_free():
+    """More checks can only reject more (never accept a rejected query); the order of the models is irrelevant;
+    a model whose threshold is -1 changes nothing."""
+    rng = np.random.default_rng(33)
+    dms = [32, 64, 48, 40]
+    keys, embs, tokens, q, las, u = _ensemble_case(rng, 300, 32, dms, 80, 4)
+    taus = [0.35, 0.45, 0.3, 0.5]
+    prev = None
+    for m in range(1, 5):
+        e = oracle.lookup_ensemble(keys, q, 0.4, embs[:m], las[:m], taus[:m], tokens, u, 4)
+        if prev is not None:
+            was_rejected = prev["decision"] == oracle.REJECT
+            assert np.all(e["decision"][was_rejected] == oracle.REJECT)
+        prev = e
+    perm = [2, 0, 3, 1]
+    p = oracle.lookup_ensemble(keys, q, 0.4, [embs[i] for i in perm], [las[i] for i in perm], [taus[i] for i in perm],
+                               tokens, u, 4)
+    np.testing.assert_array_equal(p["decision"], prev["decision"])
+    np.testing.assert_array_equal(p["resp_score"], prev["resp_score"][:, perm])
+    two = oracle.lookup_ensemble(keys, q, 0.4, embs[:2], las[:2], taus[:2], tokens, u, 4)
+    loose = oracle.lookup_ensemble(keys, q, 0.4, embs[:3], las[:3], taus[:2] + [-1.0], tokens, u, 4)
+    np.testing.assert_array_equal(two["decision"], loose["decision"])
