@@ -9,7 +9,9 @@ bfloat16 inputs, k = 16, whose inputs already sit in device memory.
 
 The headline workload (`value`) is serve_large: 4096 queries per call (the
 matrix-core-bound regime); serve_small (16 queries per call, the HBM-bound
-regime) is measured in the same run and reported under "secondary".  For
+regime) is measured in the same run and reported under "secondary", and the
+same keys with the four-model lookahead ensemble (Section 4.4) under
+"ensemble".  For
 each, "roofline" rates the stage-1 kernel, timed with HIP events recorded by
 the library on the launch stream, against the MI355X peak (bf16 dense MFMA
 2.5 PFLOP/s, HBM 8 TB/s).  "cpu_baseline" times the CPU oracle on a bounded
@@ -40,6 +42,7 @@ def parse():
     ap.add_argument("--workload", default="serve_large", choices=["serve_large", "serve_small"])
     ap.add_argument("--no-secondary", action="store_true", help="measure only the headline workload")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
+    ap.add_argument("--no-ensemble", action="store_true", help="skip the lookahead-ensemble measurement")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="per-launch HBM traffic measured with rocprofv3 counters (JSON), if present")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
@@ -195,6 +198,58 @@ def run_workload(name, steps, warmup, lc, torch, synth, traffic_db, want_cpu):
     return res
 
 
+def run_ensemble(steps, warmup, lc, torch, synth):
+    """The serve_large workload with the lookahead ensemble of Section 5.4 (four prefix models of dimensions
+    1024 / 384 / 768 / 1024, each at the threshold min(0.70, P10) of Appendix A.2, which is 0.70 for the
+    synthetic benign prefix cosines U[0.70, 0.98]); half of the benign queries carry one substituted token,
+    so the embedding checks decide them."""
+    from tests.gpu_util import gpu_ensemble_cache, to_dev
+    sp = synth.spec("serve_large")
+    dims = synth.ENSEMBLE_DIMS
+    tau_r = (0.70,) * len(dims)
+    call_b = sp.B
+    t0 = time.time()
+    w = synth.generate(sp)
+    embs = synth.ensemble_entries(sp, dims, 0, sp.N)
+    las, la_tok = synth.ensemble_lookahead(sp, dims, embs, w.tokens,
+                                           dict(cls=w.cls, target=w.target, la_tok=w.la_tok))
+    log(f"[bench] ensemble: generated in {time.time() - t0:.1f}s")
+    c = gpu_ensemble_cache(lc, sp, dims, w.keys, embs, w.tokens, max_batch=call_b, insert_chunk=1 << 18)
+    del embs
+    q = to_dev(w.queries)
+    a = [to_dev(x) for x in las]
+    t = to_dev(np.ascontiguousarray(la_tok[:, :sp.k]))
+    dev = torch.device("cuda", 0)
+    out = (torch.empty(call_b, dtype=torch.int32, device=dev), torch.empty(call_b, dtype=torch.float32, device=dev),
+           torch.empty((call_b, len(dims)), dtype=torch.float32, device=dev),
+           torch.empty(call_b, dtype=torch.int32, device=dev))
+
+    def step():
+        c.lookup_ensemble(q, a, t, sp.tau_q, tau_r, sp.k, out=out)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    dec = out[3].cpu().numpy()
+    served = np.isin(dec, [2, 3])
+    ben, col = w.cls == synth.CLS_BENIGN, w.cls == synth.CLS_COLLISION
+    res = dict(workload=f"serve_large keys with {len(dims)} prefix models of dimensions {list(dims)}, "
+                        f"tau_r {list(tau_r)}, B={call_b} queries per call",
+               m=len(dims), value=call_b / (ms * 1e-3), unit="lookups/s", ms_per_step=ms,
+               rates=dict(benign_hit_rate=float(served[ben].mean()), attack_hit_rate=float(served[col].mean())))
+    c.close()
+    del w, q, a, t
+    torch.cuda.empty_cache()
+    return res
+
+
 def cpu_baseline(sp, w, call_b):
     """The CPU oracle, as it is, on a bounded sample: a few queries against the full cache."""
     import oracle
@@ -222,17 +277,14 @@ def main():
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: the lookup is built and measured on a single MI355X; "
-              "sharding the cache over GPUs is a design note, not part of this build.", file=sys.stderr)
+              "sharding the cache over several GPUs is not implemented.", file=sys.stderr)
         sys.exit(2)
     if args.calibrate_copy_mib:
         calibrate_copy(args.calibrate_copy_mib)
         return
     import torch
     import synth
-    from paper_2608_01718_amd import build as b
-    if not os.path.exists(b.OUT):
-        b.build()
-    import paper_2608_01718_amd as lc
+    import paper_2608_01718_amd as lc  # raises if liblacache.so has not been built
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     traffic_db = {}
     if os.path.exists(args.traffic):
@@ -243,6 +295,8 @@ def main():
     if not args.no_secondary:
         other = "serve_small" if args.workload == "serve_large" else "serve_large"
         secondary = run_workload(other, args.steps, args.warmup, lc, torch, synth, traffic_db, False)
+
+    ensemble = None if args.no_ensemble else run_ensemble(args.steps, args.warmup, lc, torch, synth)
 
     line = {
         "metric": "cache lookups/sec (2-stage) at N=1M,d=768; % HBM / MFMA roofline",
@@ -270,6 +324,8 @@ def main():
             "roofline": {k: secondary["roofline"][k] for k in ("bound", "achieved", "peak", "unit", "frac",
                                                                   "traffic")},
             "stage1_kernel_avg_ms": secondary["roofline"]["kernel_avg_ms"], "rates": secondary["rates"]}
+    if ensemble:
+        line["ensemble"] = ensemble
     print(json.dumps(line), flush=True)
 
 

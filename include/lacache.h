@@ -20,6 +20,12 @@
  *     (Section 5.1: lookahead check sim(f_k(x), f_k(x')) >= tau_a).  Only
  *     when both pass is the cached response served; otherwise the caller
  *     decodes and inserts (Algorithm 1, fallback branch).
+ *   - With an ensemble of m lookahead checks (Section 4.4: m prefix
+ *     embedding models, a hit needs every check to pass) each entry stores m
+ *     prefix embeddings, one per model and each of its own dimension, and
+ *     the embedding branch of stage 2 passes only when every model's cosine
+ *     reaches that model's threshold.  The single-model functions are the
+ *     case m = 1, with the prefix model of the key's dimension.
  *
  * Conventions for every function below:
  *   - Every array argument is a DEVICE pointer on the handle's device (for
@@ -47,6 +53,9 @@ extern "C" {
 #endif
 
 typedef struct lacache_s *lacache_t;
+
+/* largest number of prefix models (lookahead checks) of an ensemble cache */
+#define LACACHE_MAX_MODELS 8
 
 /* dtype of every input vector of a cache (keys, prefix embeddings, queries, lookahead embeddings) */
 typedef enum { LACACHE_F32 = 0, LACACHE_BF16 = 1 } lacache_dtype;
@@ -81,6 +90,21 @@ enum {
 int lacache_create(lacache_t *out, int64_t capacity, int32_t d, int32_t k_cap, lacache_dtype in_dtype,
                    int32_t max_batch, int32_t device);
 
+/*
+ * Create a cache whose entries carry an ensemble of m response-prefix
+ * embeddings (Section 4.4, m lookahead checks), 1 <= m <= LACACHE_MAX_MODELS.
+ * d_resp (host, [m]) gives each prefix model's dimension, 1 .. 16384; the
+ * other arguments are those of lacache_create, which equals this call with
+ * m = 1 and d_resp = {d}.  The store takes capacity * (2 * d_pad + sum over
+ * i of 2 * d_pad_i + 4 * k_cap) bytes, d_pad_i = d_resp[i] rounded up to a
+ * multiple of 128.
+ */
+int lacache_create_ensemble(lacache_t *out, int64_t capacity, int32_t d, int32_t k_cap, lacache_dtype in_dtype,
+                            int32_t max_batch, int32_t device, int32_t m, const int32_t *d_resp);
+
+/* Number of prefix models m of the cache; -1 for a NULL handle. */
+int32_t lacache_models(lacache_t h);
+
 /* Wait for the device, free everything the handle owns, and the handle itself. NULL is a no-op. */
 int lacache_destroy(lacache_t h);
 
@@ -94,10 +118,19 @@ int lacache_destroy(lacache_t h);
  * Entries get indices size .. size+n-1 in order; *first_idx (host) receives
  * the first.  The entry count is updated immediately, so later lookups on
  * the same stream see the new entries.  n == 0 is a no-op.  Returns
- * LACACHE_EFULL, inserting nothing, if n > capacity - size.
+ * LACACHE_EFULL, inserting nothing, if n > capacity - size.  Only for a
+ * cache with m = 1 (else LACACHE_EINVAL).
  */
 int lacache_insert(lacache_t h, const void *keys, const void *resp_emb, const int32_t *resp_tokens, int32_t n,
                    int64_t *first_idx, void *stream);
+
+/*
+ * lacache_insert for any m: resp_emb is a HOST array of m device pointers,
+ * resp_emb[i] being [n][d_resp[i]] (cache dtype), the prefix embedding of
+ * each entry under model i.  Each is normalised and rounded as keys are.
+ */
+int lacache_insert_ensemble(lacache_t h, const void *keys, const void *const *resp_emb, const int32_t *resp_tokens,
+                            int32_t n, int64_t *first_idx, void *stream);
 
 /*
  * Two-stage lookup of B queries (Algorithm 1).
@@ -114,23 +147,42 @@ int lacache_insert(lacache_t h, const void *keys, const void *resp_emb, const in
  *               quiet NaN (0x7FC00000) when stage 2 did not run
  *   decision    LACACHE_MISS / REJECT / HIT / HIT_EXACT
  * Similarities are dot products of the bfloat16-rounded normalised vectors,
- * accumulated in float32.  B == 0 is a no-op.
+ * accumulated in float32.  B == 0 is a no-op.  Only for a cache with m = 1
+ * (else LACACHE_EINVAL).
  */
 int lacache_lookup(lacache_t h, const void *queries, const void *lookahead_emb, const int32_t *lookahead_tokens,
                    int32_t B, float tau_q, float tau_r, int32_t k, int32_t *idx, float *score, float *resp_score,
                    int32_t *decision, void *stream);
 
+/*
+ * lacache_lookup for any m (Section 4.4 ensemble):
+ *   lookahead_emb  HOST array of m device pointers, lookahead_emb[i] being
+ *                  [B][d_resp[i]] (cache dtype): the lookahead prefix under model i
+ *   tau_r          HOST array of m finite stage-2 thresholds, one per model
+ *   resp_score     [B][m]: cosine of each model's prefix embeddings, clamped to
+ *                  [-1, 1]; quiet NaN in every column when stage 2 did not run
+ * decision is HIT_EXACT when the k tokens are identical, HIT when every
+ * model's cosine is >= its tau_r[i], REJECT otherwise, MISS on a stage-1
+ * miss.  Every other argument and output is as in lacache_lookup.
+ */
+int lacache_lookup_ensemble(lacache_t h, const void *queries, const void *const *lookahead_emb,
+                            const int32_t *lookahead_tokens, int32_t B, float tau_q, const float *tau_r, int32_t k,
+                            int32_t *idx, float *score, float *resp_score, int32_t *decision, void *stream);
+
 /* Number of entries inserted so far (host-side count); -1 for a NULL handle. */
 int64_t lacache_size(lacache_t h);
 
 /*
- * Copy entries first .. first+n-1 of the store out, as stored: keys_bf16 and
- * emb_bf16 are [n][d] bfloat16 bit patterns, tokens [n][k_cap] int32.  Any of
- * the three may be NULL to skip it.  Requires 0 <= first, n >= 0,
- * first + n <= size.  For inspection and tests.
+ * Copy entries first .. first+n-1 of the store out, as stored: keys_bf16 is
+ * [n][d] and emb_bf16 [n][d_resp[0]] bfloat16 bit patterns (prefix model 0),
+ * tokens [n][k_cap] int32.  Any of the three may be NULL to skip it.
+ * Requires 0 <= first, n >= 0, first + n <= size.  For inspection and tests.
  */
 int lacache_export(lacache_t h, int64_t first, int32_t n, uint16_t *keys_bf16, uint16_t *emb_bf16, int32_t *tokens,
                    void *stream);
+
+/* As lacache_export, for the stored prefix embeddings of model 0 <= model < m: emb_bf16 is [n][d_resp[model]]. */
+int lacache_export_prefix(lacache_t h, int32_t model, int64_t first, int32_t n, uint16_t *emb_bf16, void *stream);
 
 /*
  * Batch-size crossover of stage 1: batches of at most b_small queries use the

@@ -4,7 +4,7 @@ Every function mirrors one entry point of ``include/lacache.h`` under the
 same name and passes torch device tensors' data pointers and the current HIP
 stream straight through; all work runs in the library's kernels.  There is no
 fallback: importing this module fails if ``liblacache.so`` has not been built
-(``python -m paper_2608_01718_amd.build``).
+(``python paper_2608_01718_amd/build.py``).
 """
 from __future__ import annotations
 
@@ -19,14 +19,23 @@ LIB_PATH = os.path.join(_HERE, "liblacache.so")
 MISS, REJECT, HIT, HIT_EXACT = 0, 1, 2, 3
 OK, EINVAL, EFULL, ENOMEM, EHIP = 0, -1, -2, -3, -4
 F32, BF16 = 0, 1
+MAX_MODELS = 8
 
 if not os.path.exists(LIB_PATH):
-    raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2608_01718_amd.build` "
+    raise ImportError(f"{LIB_PATH} is missing: build it with `python paper_2608_01718_amd/build.py` "
                       "(there is no non-HIP implementation of the lookup)")
 
 _lib = ctypes.CDLL(LIB_PATH)
 _P, _i32, _i64, _f32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float
 _lib.lacache_create.argtypes = [ctypes.POINTER(_P), _i64, _i32, _i32, ctypes.c_int, _i32, _i32]
+_lib.lacache_create_ensemble.argtypes = [ctypes.POINTER(_P), _i64, _i32, _i32, ctypes.c_int, _i32, _i32, _i32,
+                                         ctypes.POINTER(_i32)]
+_lib.lacache_models.argtypes = [_P]
+_lib.lacache_models.restype = _i32
+_lib.lacache_insert_ensemble.argtypes = [_P, _P, ctypes.POINTER(_P), _P, _i32, ctypes.POINTER(_i64), _P]
+_lib.lacache_lookup_ensemble.argtypes = [_P, _P, ctypes.POINTER(_P), _P, _i32, _f32, ctypes.POINTER(_f32), _i32,
+                                         _P, _P, _P, _P, _P]
+_lib.lacache_export_prefix.argtypes = [_P, _i32, _i64, _i32, _P, _P]
 _lib.lacache_destroy.argtypes = [_P]
 _lib.lacache_insert.argtypes = [_P, _P, _P, _P, _i32, ctypes.POINTER(_i64), _P]
 _lib.lacache_lookup.argtypes = [_P, _P, _P, _P, _i32, _f32, _f32, _i32, _P, _P, _P, _P, _P]
@@ -39,9 +48,10 @@ _lib.lacache_profile_read.argtypes = [_P, ctypes.POINTER(ctypes.c_double), ctype
 _lib.lacache_strerror.argtypes = [ctypes.c_int]
 _lib.lacache_strerror.restype = ctypes.c_char_p
 
-EXPORTED = ("lacache_create", "lacache_destroy", "lacache_insert", "lacache_lookup", "lacache_size",
-            "lacache_export", "lacache_set_small_batch", "lacache_profile", "lacache_profile_read",
-            "lacache_strerror")
+EXPORTED = ("lacache_create", "lacache_create_ensemble", "lacache_models", "lacache_destroy", "lacache_insert",
+            "lacache_insert_ensemble", "lacache_lookup", "lacache_lookup_ensemble", "lacache_size",
+            "lacache_export", "lacache_export_prefix", "lacache_set_small_batch", "lacache_profile",
+            "lacache_profile_read", "lacache_strerror")
 
 
 class LaCacheError(RuntimeError):
@@ -83,16 +93,29 @@ def _ints(t: torch.Tensor, shape, device: int, name: str) -> int:
 
 
 class LaCache:
-    """A handle of the C library plus the sizes it was created with."""
+    """A handle of the C library plus the sizes it was created with.  ``d_resp`` (one dimension per prefix
+    model) makes an ensemble cache through lacache_create_ensemble; without it the cache has one prefix
+    model of dimension d."""
 
     def __init__(self, capacity: int, d: int, k_cap: int, in_dtype: int = BF16, max_batch: int = 4096,
-                 device: int = 0):
+                 device: int = 0, d_resp=None):
         self.capacity, self.d, self.k_cap, self.in_dtype = capacity, d, k_cap, in_dtype
         self.max_batch, self.device = max_batch, device
         h = _P()
-        _check(_lib.lacache_create(ctypes.byref(h), capacity, d, k_cap, in_dtype, max_batch, device),
-               "lacache_create")
+        if d_resp is None:
+            self.d_resp = (d,)
+            _check(_lib.lacache_create(ctypes.byref(h), capacity, d, k_cap, in_dtype, max_batch, device),
+                   "lacache_create")
+        else:
+            self.d_resp = tuple(int(x) for x in d_resp)
+            arr = (_i32 * max(1, len(self.d_resp)))(*self.d_resp)
+            _check(_lib.lacache_create_ensemble(ctypes.byref(h), capacity, d, k_cap, in_dtype, max_batch, device,
+                                                len(self.d_resp), arr), "lacache_create_ensemble")
         self._h = h
+
+    @property
+    def m(self) -> int:
+        return len(self.d_resp)
 
     @property
     def handle(self):
@@ -108,6 +131,16 @@ class LaCache:
 
     def export(self, first: int, n: int, stream=None):
         return lacache_export(self, first, n, stream)
+
+    def insert_ensemble(self, keys, resp_embs, resp_tokens, stream=None) -> int:
+        return lacache_insert_ensemble(self, keys, resp_embs, resp_tokens, stream)
+
+    def lookup_ensemble(self, queries, lookahead_embs, lookahead_tokens, tau_q, tau_r, k, out=None, stream=None):
+        return lacache_lookup_ensemble(self, queries, lookahead_embs, lookahead_tokens, tau_q, tau_r, k, out,
+                                       stream)
+
+    def export_prefix(self, model: int, first: int, n: int, stream=None):
+        return lacache_export_prefix(self, model, first, n, stream)
 
     def size(self) -> int:
         return lacache_size(self)
@@ -137,6 +170,15 @@ def lacache_create(capacity: int, d: int, k_cap: int, in_dtype: int = BF16, max_
     return LaCache(capacity, d, k_cap, in_dtype, max_batch, device)
 
 
+def lacache_create_ensemble(capacity: int, d: int, k_cap: int, in_dtype: int, max_batch: int, device: int,
+                            d_resp) -> LaCache:
+    return LaCache(capacity, d, k_cap, in_dtype, max_batch, device, d_resp=d_resp)
+
+
+def lacache_models(c: LaCache) -> int:
+    return int(_lib.lacache_models(c.handle))
+
+
 def lacache_destroy(c: LaCache) -> None:
     h, c._h = c._h, None
     _check(_lib.lacache_destroy(h), "lacache_destroy")
@@ -150,6 +192,48 @@ def lacache_insert(c: LaCache, keys, resp_emb, resp_tokens, stream=None) -> int:
                                _ints(resp_tokens, (n, c.k_cap), c.device, "resp_tokens"), n, ctypes.byref(first),
                                _stream(c.device, stream)), "lacache_insert")
     return first.value
+
+
+def lacache_insert_ensemble(c: LaCache, keys, resp_embs, resp_tokens, stream=None) -> int:
+    """resp_embs: one [n][d_resp[i]] tensor per prefix model."""
+    n = keys.shape[0]
+    if len(resp_embs) != c.m:
+        raise ValueError(f"resp_embs: expected {c.m} tensors, got {len(resp_embs)}")
+    ptrs = (_P * c.m)(*[_vec(e, c.in_dtype, n, c.d_resp[i], c.device, f"resp_embs[{i}]")
+                         for i, e in enumerate(resp_embs)])
+    first = _i64(-1)
+    _check(_lib.lacache_insert_ensemble(c.handle, _vec(keys, c.in_dtype, n, c.d, c.device, "keys"), ptrs,
+                                        _ints(resp_tokens, (n, c.k_cap), c.device, "resp_tokens"), n,
+                                        ctypes.byref(first), _stream(c.device, stream)), "lacache_insert_ensemble")
+    return first.value
+
+
+def lacache_lookup_ensemble(c: LaCache, queries, lookahead_embs, lookahead_tokens, tau_q: float, tau_r, k: int,
+                            out=None, stream=None):
+    """lookahead_embs: one [B][d_resp[i]] tensor per prefix model; tau_r: one threshold per model.
+    Returns (idx int32 [B], score f32 [B], resp_score f32 [B][m], decision int32 [B])."""
+    B = queries.shape[0]
+    m = c.m
+    dev = torch.device("cuda", c.device)
+    if len(lookahead_embs) != m or len(tau_r) != m:
+        raise ValueError(f"expected {m} lookahead embeddings and {m} thresholds")
+    if out is None:
+        out = (torch.empty(B, dtype=torch.int32, device=dev), torch.empty(B, dtype=torch.float32, device=dev),
+               torch.empty((B, m), dtype=torch.float32, device=dev), torch.empty(B, dtype=torch.int32, device=dev))
+    idx, score, resp, dec = out
+    for t, dt, n, nm in ((idx, torch.int32, B, "idx"), (score, torch.float32, B, "score"),
+                         (resp, torch.float32, B * m, "resp"), (dec, torch.int32, B, "decision")):
+        if t.dtype != dt or t.device != dev or t.numel() != n or not t.is_contiguous():
+            raise ValueError(f"{nm}: expected a contiguous {dt} tensor of {n} elements on {dev}")
+    ptrs = (_P * m)(*[_vec(e, c.in_dtype, B, c.d_resp[i], c.device, f"lookahead_embs[{i}]")
+                      for i, e in enumerate(lookahead_embs)])
+    taus = (_f32 * m)(*[float(t) for t in tau_r])
+    _check(_lib.lacache_lookup_ensemble(c.handle, _vec(queries, c.in_dtype, B, c.d, c.device, "queries"), ptrs,
+                                        _ints(lookahead_tokens, (B, k), c.device, "lookahead_tokens"), B,
+                                        float(tau_q), taus, int(k), idx.data_ptr(), score.data_ptr(),
+                                        resp.data_ptr(), dec.data_ptr(), _stream(c.device, stream)),
+           "lacache_lookup_ensemble")
+    return out
 
 
 def lacache_lookup(c: LaCache, queries, lookahead_emb, lookahead_tokens, tau_q: float, tau_r: float, k: int,
@@ -181,11 +265,21 @@ def lacache_export(c: LaCache, first: int, n: int, stream=None):
     """Returns (keys bf16-bits int16 [n][d], emb int16 [n][d], tokens int32 [n][k_cap]) as stored."""
     dev = torch.device("cuda", c.device)
     keys = torch.empty((n, c.d), dtype=torch.int16, device=dev)
-    emb = torch.empty((n, c.d), dtype=torch.int16, device=dev)
+    emb = torch.empty((n, c.d_resp[0]), dtype=torch.int16, device=dev)
     tok = torch.empty((n, c.k_cap), dtype=torch.int32, device=dev)
     _check(_lib.lacache_export(c.handle, first, n, keys.data_ptr(), emb.data_ptr(), tok.data_ptr(),
                                _stream(c.device, stream)), "lacache_export")
     return keys, emb, tok
+
+
+def lacache_export_prefix(c: LaCache, model: int, first: int, n: int, stream=None):
+    """The stored prefix embeddings of one model, bf16 bits as int16 [n][d_resp[model]]."""
+    if not 0 <= model < c.m:
+        raise ValueError(f"model must be in [0, {c.m})")
+    emb = torch.empty((n, c.d_resp[model]), dtype=torch.int16, device=torch.device("cuda", c.device))
+    _check(_lib.lacache_export_prefix(c.handle, model, first, n, emb.data_ptr(), _stream(c.device, stream)),
+           "lacache_export_prefix")
+    return emb
 
 
 def lacache_set_small_batch(c: LaCache, b_small: int) -> None:

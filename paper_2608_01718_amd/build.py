@@ -1,6 +1,6 @@
 """Build liblacache.so (the C-ABI library) for gfx950 with hipcc, in-tree.
 
-    python -m paper_2608_01718_amd.build
+    python paper_2608_01718_amd/build.py
 """
 from __future__ import annotations
 

@@ -7,7 +7,9 @@
 // first k token IDs (Section 4.2, cache structure <h(x), [h(f_k(x)), f(x)]>)
 // -- is gathered and compared with the query's lookahead.  The check passes
 // on identical tokens, or on a prefix-embedding cosine >= tau_r (Section 5.1,
-// lookahead check).  Decisions: 0 MISS, 1 REJECT, 2 HIT, 3 HIT_EXACT.
+// lookahead check) -- under every one of the m prefix models when the cache
+// holds an ensemble of lookahead checks (Section 4.4).  Decisions: 0 MISS,
+// 1 REJECT, 2 HIT, 3 HIT_EXACT.
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -43,10 +45,10 @@ __device__ int32_t replay_group(const u32x4* __restrict__ keys, const u32x4* __r
 
 __global__ __launch_bounds__(256) void k_finalize_verify(
     const uint64_t* __restrict__ part, int P, int part_groups, const u32x4* __restrict__ keys_tiled,
-    const u32x4* __restrict__ qt, int kc, int B, int n_rows, const void* __restrict__ la, int dtype, int d,
-    const int32_t* __restrict__ la_tok, int k, const uint16_t* __restrict__ emb, int d_pad,
-    const int32_t* __restrict__ tokens, int k_cap, float tau_q, float tau_r, int32_t* __restrict__ idx_out,
-    float* __restrict__ score_out, float* __restrict__ resp_out, int32_t* __restrict__ dec_out) {
+    const u32x4* __restrict__ qt, int kc, int B, int n_rows, int dtype, const PrefixModels M,
+    const int32_t* __restrict__ la_tok, int k, const int32_t* __restrict__ tokens, int k_cap, float tau_q,
+    int32_t* __restrict__ idx_out, float* __restrict__ score_out, float* __restrict__ resp_out,
+    int32_t* __restrict__ dec_out) {
     const int lane = threadIdx.x & 63;
     const int b = blockIdx.x * 4 + (threadIdx.x >> 6);
     if (b >= B) return;
@@ -55,9 +57,9 @@ __global__ __launch_bounds__(256) void k_finalize_verify(
         if (lane == 0) {
             idx_out[b] = -1;
             score_out[b] = qnan;
-            resp_out[b] = qnan;
             dec_out[b] = 0;
         }
+        if (lane < M.m) resp_out[(int64_t)b * M.m + lane] = qnan;
         return;
     }
     uint64_t m = 0;
@@ -72,28 +74,36 @@ __global__ __launch_bounds__(256) void k_finalize_verify(
         if (lane == 0) {
             idx_out[b] = (m == 0ull) ? -1 : i;
             score_out[b] = (m == 0ull) ? qnan : score;
-            resp_out[b] = qnan;
             dec_out[b] = 0;
         }
+        if (lane < M.m) resp_out[(int64_t)b * M.m + lane] = qnan;
         return;
     }
 
-    // normalise the lookahead embedding exactly as stored vectors are, and dot it with the entry's prefix row
-    const char* src = (const char*)la + (int64_t)b * d * (dtype == 0 ? 4 : 2);
-    const u32x4* er = (const u32x4*)(emb + (int64_t)i * d_pad);
-    float acc = 0.0f;
-    normalise_row(src, dtype, d, d_pad, true, lane, [&](int j0, u32x4 w) {
-        const u32x4 e = er[j0 >> 3];
-        const uint32_t av[4] = {w.x, w.y, w.z, w.w}, ev[4] = {e.x, e.y, e.z, e.w};
+    // for every prefix model: normalise the lookahead embedding exactly as stored vectors are and dot it with
+    // the entry's stored prefix row; the embedding check passes only if every model reaches its threshold
+    // (Section 4.4: with m lookahead checks a hit needs all of them)
+    const size_t esz = dtype == 0 ? 4 : 2;
+    bool all_pass = true;
+    for (int mi = 0; mi < M.m; ++mi) {
+        const char* src = (const char*)M.la[mi] + (int64_t)b * M.d[mi] * esz;
+        const u32x4* er = (const u32x4*)(M.emb[mi] + (int64_t)i * M.d_pad[mi]);
+        float acc = 0.0f;
+        normalise_row(src, dtype, M.d[mi], M.d_pad[mi], true, lane, [&](int j0, u32x4 w) {
+            const u32x4 e = er[j0 >> 3];
+            const uint32_t av[4] = {w.x, w.y, w.z, w.w}, ev[4] = {e.x, e.y, e.z, e.w};
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
-            // bf16 x bf16 products are exact in float; padded columns are zero on both sides
-            acc += __uint_as_float(av[t] << 16) * __uint_as_float(ev[t] << 16);
-            acc += __uint_as_float(av[t] & 0xFFFF0000u) * __uint_as_float(ev[t] & 0xFFFF0000u);
-        }
-    });
-    acc = wave_sum_f32(acc);
-    const float r = fminf(fmaxf(acc, -1.0f), 1.0f);
+            for (int t = 0; t < 4; ++t) {
+                // bf16 x bf16 products are exact in float; padded columns are zero on both sides
+                acc += __uint_as_float(av[t] << 16) * __uint_as_float(ev[t] << 16);
+                acc += __uint_as_float(av[t] & 0xFFFF0000u) * __uint_as_float(ev[t] & 0xFFFF0000u);
+            }
+        });
+        acc = wave_sum_f32(acc);
+        const float r = fminf(fmaxf(acc, -1.0f), 1.0f);
+        if (lane == 0) resp_out[(int64_t)b * M.m + mi] = r;
+        all_pass = all_pass && (r >= M.tau[mi]);
+    }
 
     // first k tokens: lane j compares token j, 64 at a time
     bool tok_eq = true;
@@ -107,20 +117,20 @@ __global__ __launch_bounds__(256) void k_finalize_verify(
     if (lane == 0) {
         idx_out[b] = i;
         score_out[b] = score;
-        resp_out[b] = r;
-        dec_out[b] = tok_eq ? 3 : (r >= tau_r ? 2 : 1);
+        dec_out[b] = tok_eq ? 3 : (all_pass ? 2 : 1);
     }
 }
 
 hipError_t launch_finalize_verify(const uint64_t* part, int P, bool part_groups, const uint16_t* keys_tiled,
-                                  const uint16_t* qt, int B, int n_rows, const void* la, int dtype, int d,
-                                  const int32_t* la_tok, int k, const uint16_t* emb, int d_pad,
-                                  const int32_t* tokens, int k_cap, float tau_q, float tau_r, int32_t* idx,
-                                  float* score, float* resp_score, int32_t* decision, hipStream_t s) {
+                                  const uint16_t* qt, int B, int n_rows, int dtype, int d_keys,
+                                  const PrefixModels& models, const int32_t* la_tok, int k, const int32_t* tokens,
+                                  int k_cap, float tau_q, int32_t* idx, float* score, float* resp_score,
+                                  int32_t* decision, hipStream_t s) {
     if (B <= 0) return hipSuccess;
+    const int d_pad = (d_keys + 127) / 128 * 128;
     k_finalize_verify<<<dim3((B + 3) / 4), dim3(256), 0, s>>>(
-        part, P, part_groups ? 1 : 0, (const u32x4*)keys_tiled, (const u32x4*)qt, d_pad / 32, B, n_rows, la, dtype,
-        d, la_tok, k, emb, d_pad, tokens, k_cap, tau_q, tau_r, idx, score, resp_score, decision);
+        part, P, part_groups ? 1 : 0, (const u32x4*)keys_tiled, (const u32x4*)qt, d_pad / 32, B, n_rows, dtype,
+        models, la_tok, k, tokens, k_cap, tau_q, idx, score, resp_score, decision);
     return hipGetLastError();
 }
 

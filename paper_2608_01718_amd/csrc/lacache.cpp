@@ -22,8 +22,10 @@ struct lacache_s {
     int64_t cap = 0, cap_pad = 0, size = 0;
     int d = 0, d_pad = 0, k_cap = 0, dtype = 0, max_batch = 0, mb_pad = 0;
     int num_cu = 0, b_small = 64;
+    int m = 1;                 // prefix models (lookahead checks) per entry
+    int d_resp[kMaxModels] = {}, d_pad_resp[kMaxModels] = {};
     uint16_t* keys = nullptr;  // tiled [cap_pad][d_pad]
-    uint16_t* emb = nullptr;   // row-major [cap][d_pad]
+    uint16_t* emb[kMaxModels] = {};  // row-major [cap][d_pad_resp[i]], one per prefix model
     int32_t* tokens = nullptr; // [cap][k_cap]
     uint16_t* qt = nullptr;    // tiled [mb_pad][d_pad] normalised queries
     uint64_t* part = nullptr;  // [max_batch][kMaxPartials] packed top-1 candidates
@@ -53,7 +55,7 @@ struct DeviceGuard {
 
 void free_all(lacache_s* h) {
     (void)hipFree(h->keys);
-    (void)hipFree(h->emb);
+    for (int i = 0; i < kMaxModels; ++i) (void)hipFree(h->emb[i]);
     (void)hipFree(h->tokens);
     (void)hipFree(h->qt);
     (void)hipFree(h->part);
@@ -96,13 +98,16 @@ const char* lacache_strerror(int code) {
     }
 }
 
-int lacache_create(lacache_t* out, int64_t capacity, int32_t d, int32_t k_cap, lacache_dtype in_dtype,
-                   int32_t max_batch, int32_t device) {
+int lacache_create_ensemble(lacache_t* out, int64_t capacity, int32_t d, int32_t k_cap, lacache_dtype in_dtype,
+                            int32_t max_batch, int32_t device, int32_t m, const int32_t* d_resp) {
     if (!out) return LACACHE_EINVAL;
     *out = nullptr;
     if (capacity < 1 || capacity > kMaxCapacity || d < 1 || d > 16384 || k_cap < 1 || k_cap > 4096 ||
-        (in_dtype != LACACHE_F32 && in_dtype != LACACHE_BF16) || max_batch < 1 || max_batch > 65536 || device < 0)
+        (in_dtype != LACACHE_F32 && in_dtype != LACACHE_BF16) || max_batch < 1 || max_batch > 65536 ||
+        device < 0 || m < 1 || m > kMaxModels || !d_resp)
         return LACACHE_EINVAL;
+    for (int i = 0; i < m; ++i)
+        if (d_resp[i] < 1 || d_resp[i] > 16384) return LACACHE_EINVAL;
     int ndev = 0;
     if (hipGetDeviceCount(&ndev) != hipSuccess) {
         (void)hipGetLastError();
@@ -119,6 +124,11 @@ int lacache_create(lacache_t* out, int64_t capacity, int32_t d, int32_t k_cap, l
     h->cap_pad = round_up(capacity, kRowTile);
     h->d = d;
     h->d_pad = (int)round_up(d, 128);
+    h->m = m;
+    for (int i = 0; i < m; ++i) {
+        h->d_resp[i] = d_resp[i];
+        h->d_pad_resp[i] = (int)round_up(d_resp[i], 128);
+    }
     h->k_cap = k_cap;
     h->dtype = (int)in_dtype;
     h->max_batch = max_batch;
@@ -133,7 +143,8 @@ int lacache_create(lacache_t* out, int64_t capacity, int32_t d, int32_t k_cap, l
 
     int rc = LACACHE_OK;
     if (rc == LACACHE_OK) rc = alloc_zero((void**)&h->keys, (size_t)h->cap_pad * h->d_pad * 2);
-    if (rc == LACACHE_OK) rc = alloc_zero((void**)&h->emb, (size_t)h->cap * h->d_pad * 2);
+    for (int i = 0; i < m && rc == LACACHE_OK; ++i)
+        rc = alloc_zero((void**)&h->emb[i], (size_t)h->cap * h->d_pad_resp[i] * 2);
     if (rc == LACACHE_OK) rc = alloc_zero((void**)&h->tokens, (size_t)h->cap * h->k_cap * 4);
     if (rc == LACACHE_OK) rc = alloc_zero((void**)&h->qt, (size_t)h->mb_pad * h->d_pad * 2);
     if (rc == LACACHE_OK) rc = alloc_zero((void**)&h->part, (size_t)h->max_batch * kMaxPartials * 8);
@@ -145,6 +156,11 @@ int lacache_create(lacache_t* out, int64_t capacity, int32_t d, int32_t k_cap, l
     }
     *out = h;
     return LACACHE_OK;
+}
+
+int lacache_create(lacache_t* out, int64_t capacity, int32_t d, int32_t k_cap, lacache_dtype in_dtype,
+                   int32_t max_batch, int32_t device) {
+    return lacache_create_ensemble(out, capacity, d, k_cap, in_dtype, max_batch, device, 1, &d);
 }
 
 int lacache_destroy(lacache_t h) {
@@ -161,14 +177,16 @@ int lacache_destroy(lacache_t h) {
 
 int64_t lacache_size(lacache_t h) { return h ? h->size : -1; }
 
-int lacache_insert(lacache_t h, const void* keys, const void* resp_emb, const int32_t* resp_tokens, int32_t n,
-                   int64_t* first_idx, void* stream) {
+int lacache_insert_ensemble(lacache_t h, const void* keys, const void* const* resp_emb, const int32_t* resp_tokens,
+                            int32_t n, int64_t* first_idx, void* stream) {
     if (!h || n < 0) return LACACHE_EINVAL;
     if (n == 0) {
         if (first_idx) *first_idx = h->size;
         return LACACHE_OK;
     }
     if (!keys || !resp_emb || !resp_tokens) return LACACHE_EINVAL;
+    for (int i = 0; i < h->m; ++i)
+        if (!resp_emb[i]) return LACACHE_EINVAL;
     if ((int64_t)n > h->cap - h->size) return LACACHE_EFULL;
     DeviceGuard g(h->device);
     if (!g.ok) return LACACHE_EHIP;
@@ -176,8 +194,10 @@ int lacache_insert(lacache_t h, const void* keys, const void* resp_emb, const in
     const int64_t first = h->size;
     if (launch_normalise(keys, h->dtype, n, n, h->d, h->d_pad, h->keys, first, true, s) != hipSuccess)
         return LACACHE_EHIP;
-    if (launch_normalise(resp_emb, h->dtype, n, n, h->d, h->d_pad, h->emb, first, false, s) != hipSuccess)
-        return LACACHE_EHIP;
+    for (int i = 0; i < h->m; ++i)
+        if (launch_normalise(resp_emb[i], h->dtype, n, n, h->d_resp[i], h->d_pad_resp[i], h->emb[i], first, false,
+                             s) != hipSuccess)
+            return LACACHE_EHIP;
     if (hipMemcpyAsync(h->tokens + first * h->k_cap, resp_tokens, (size_t)n * h->k_cap * 4,
                        hipMemcpyDeviceToDevice, s) != hipSuccess)
         return LACACHE_EHIP;
@@ -186,8 +206,14 @@ int lacache_insert(lacache_t h, const void* keys, const void* resp_emb, const in
     return LACACHE_OK;
 }
 
-static int lookup_chunk(lacache_t h, const char* queries, const char* la, const int32_t* la_tok, int B, float tau_q,
-                        float tau_r, int k, int32_t* idx, float* score, float* resp, int32_t* dec, hipStream_t s) {
+int lacache_insert(lacache_t h, const void* keys, const void* resp_emb, const int32_t* resp_tokens, int32_t n,
+                   int64_t* first_idx, void* stream) {
+    if (h && h->m != 1) return LACACHE_EINVAL;
+    return lacache_insert_ensemble(h, keys, &resp_emb, resp_tokens, n, first_idx, stream);
+}
+
+static int lookup_chunk(lacache_t h, const char* queries, const PrefixModels& models, const int32_t* la_tok, int B,
+                        float tau_q, int k, int32_t* idx, float* score, float* resp, int32_t* dec, hipStream_t s) {
     const int n_rows = (int)h->size;
     int P = 0;
     const bool small = B <= h->b_small;
@@ -206,32 +232,51 @@ static int lookup_chunk(lacache_t h, const char* queries, const char* la, const 
         if (e != hipSuccess) return LACACHE_EHIP;
         if (h->profiling && hipEventRecord(e1, s) != hipSuccess) return LACACHE_EHIP;
     }
-    if (launch_finalize_verify(h->part, P, !small, h->keys, h->qt, B, n_rows, la, h->dtype, h->d, la_tok, k, h->emb,
-                               h->d_pad, h->tokens, h->k_cap, tau_q, tau_r, idx, score, resp, dec, s) != hipSuccess)
+    if (launch_finalize_verify(h->part, P, !small, h->keys, h->qt, B, n_rows, h->dtype, h->d, models, la_tok, k,
+                               h->tokens, h->k_cap, tau_q, idx, score, resp, dec, s) != hipSuccess)
         return LACACHE_EHIP;
+    return LACACHE_OK;
+}
+
+int lacache_lookup_ensemble(lacache_t h, const void* queries, const void* const* lookahead_emb,
+                            const int32_t* lookahead_tokens, int32_t B, float tau_q, const float* tau_r, int32_t k,
+                            int32_t* idx, float* score, float* resp_score, int32_t* decision, void* stream) {
+    if (!h || B < 0 || k < 1 || k > h->k_cap || !std::isfinite(tau_q) || !tau_r) return LACACHE_EINVAL;
+    for (int i = 0; i < h->m; ++i)
+        if (!std::isfinite(tau_r[i])) return LACACHE_EINVAL;
+    if (B == 0) return LACACHE_OK;
+    if (!queries || !lookahead_emb || !lookahead_tokens || !idx || !score || !resp_score || !decision)
+        return LACACHE_EINVAL;
+    for (int i = 0; i < h->m; ++i)
+        if (!lookahead_emb[i]) return LACACHE_EINVAL;
+    DeviceGuard g(h->device);
+    if (!g.ok) return LACACHE_EHIP;
+    const size_t esz = h->dtype == LACACHE_F32 ? 4 : 2;
+    for (int b0 = 0; b0 < B; b0 += h->max_batch) {
+        const int nb = (B - b0) < h->max_batch ? (B - b0) : h->max_batch;
+        PrefixModels models{};
+        models.m = h->m;
+        for (int i = 0; i < h->m; ++i) {
+            models.la[i] = (const char*)lookahead_emb[i] + (size_t)b0 * h->d_resp[i] * esz;
+            models.emb[i] = h->emb[i];
+            models.d[i] = h->d_resp[i];
+            models.d_pad[i] = h->d_pad_resp[i];
+            models.tau[i] = tau_r[i];
+        }
+        const int rc = lookup_chunk(h, (const char*)queries + (size_t)b0 * h->d * esz, models,
+                                    lookahead_tokens + (size_t)b0 * k, nb, tau_q, k, idx + b0, score + b0,
+                                    resp_score + (size_t)b0 * h->m, decision + b0, (hipStream_t)stream);
+        if (rc != LACACHE_OK) return rc;
+    }
     return LACACHE_OK;
 }
 
 int lacache_lookup(lacache_t h, const void* queries, const void* lookahead_emb, const int32_t* lookahead_tokens,
                    int32_t B, float tau_q, float tau_r, int32_t k, int32_t* idx, float* score, float* resp_score,
                    int32_t* decision, void* stream) {
-    if (!h || B < 0 || k < 1 || k > h->k_cap || !std::isfinite(tau_q) || !std::isfinite(tau_r))
-        return LACACHE_EINVAL;
-    if (B == 0) return LACACHE_OK;
-    if (!queries || !lookahead_emb || !lookahead_tokens || !idx || !score || !resp_score || !decision)
-        return LACACHE_EINVAL;
-    DeviceGuard g(h->device);
-    if (!g.ok) return LACACHE_EHIP;
-    const size_t esz = h->dtype == LACACHE_F32 ? 4 : 2;
-    for (int b0 = 0; b0 < B; b0 += h->max_batch) {
-        const int nb = (B - b0) < h->max_batch ? (B - b0) : h->max_batch;
-        const int rc = lookup_chunk(h, (const char*)queries + (size_t)b0 * h->d * esz,
-                                    (const char*)lookahead_emb + (size_t)b0 * h->d * esz,
-                                    lookahead_tokens + (size_t)b0 * k, nb, tau_q, tau_r, k, idx + b0, score + b0,
-                                    resp_score + b0, decision + b0, (hipStream_t)stream);
-        if (rc != LACACHE_OK) return rc;
-    }
-    return LACACHE_OK;
+    if (h && h->m != 1) return LACACHE_EINVAL;
+    return lacache_lookup_ensemble(h, queries, &lookahead_emb, lookahead_tokens, B, tau_q, &tau_r, k, idx, score,
+                                   resp_score, decision, stream);
 }
 
 int lacache_export(lacache_t h, int64_t first, int32_t n, uint16_t* keys_bf16, uint16_t* emb_bf16, int32_t* tokens,
@@ -243,13 +288,28 @@ int lacache_export(lacache_t h, int64_t first, int32_t n, uint16_t* keys_bf16, u
     hipStream_t s = (hipStream_t)stream;
     if (keys_bf16 && launch_export(h->keys, first, n, h->d, h->d_pad, keys_bf16, true, s) != hipSuccess)
         return LACACHE_EHIP;
-    if (emb_bf16 && launch_export(h->emb, first, n, h->d, h->d_pad, emb_bf16, false, s) != hipSuccess)
+    if (emb_bf16 && launch_export(h->emb[0], first, n, h->d_resp[0], h->d_pad_resp[0], emb_bf16, false, s) !=
+                        hipSuccess)
         return LACACHE_EHIP;
     if (tokens && hipMemcpyAsync(tokens, h->tokens + first * h->k_cap, (size_t)n * h->k_cap * 4,
                                  hipMemcpyDeviceToDevice, s) != hipSuccess)
         return LACACHE_EHIP;
     return LACACHE_OK;
 }
+
+int lacache_export_prefix(lacache_t h, int32_t model, int64_t first, int32_t n, uint16_t* emb_bf16, void* stream) {
+    if (!h || model < 0 || model >= h->m || first < 0 || n < 0 || first + n > h->size) return LACACHE_EINVAL;
+    if (n == 0) return LACACHE_OK;
+    if (!emb_bf16) return LACACHE_EINVAL;
+    DeviceGuard g(h->device);
+    if (!g.ok) return LACACHE_EHIP;
+    if (launch_export(h->emb[model], first, n, h->d_resp[model], h->d_pad_resp[model], emb_bf16, false,
+                      (hipStream_t)stream) != hipSuccess)
+        return LACACHE_EHIP;
+    return LACACHE_OK;
+}
+
+int32_t lacache_models(lacache_t h) { return h ? h->m : -1; }
 
 int lacache_set_small_batch(lacache_t h, int32_t b_small) {
     if (!h || b_small < 0 || b_small > 16 * stream_max_qg(h->d_pad)) return LACACHE_EINVAL;

@@ -31,13 +31,23 @@ hipError_t launch_stage1_stream(const uint16_t* keys, const uint16_t* qt, int B,
 hipError_t launch_stage1_gemm(const uint16_t* keys, const uint16_t* qt, int B, int n_rows, int d_pad,
                               uint64_t* part, int num_cu, int* P_out, hipStream_t s);
 
+// The response-prefix embedding models of stage 2 (one per lookahead check of an ensemble).
+constexpr int kMaxModels = 8;
+struct PrefixModels {
+    int m;                             // number of models, 1 .. kMaxModels
+    const void* la[kMaxModels];        // [B][d_i] lookahead embeddings of the batch (cache dtype)
+    const uint16_t* emb[kMaxModels];   // [capacity][d_pad_i] stored normalised prefix embeddings
+    int d[kMaxModels], d_pad[kMaxModels];
+    float tau[kMaxModels];             // stage-2 threshold of each model
+};
+
 // Merge the P partial candidates of each query (rows, or 32-row groups to replay against keys_tiled and
-// the tiled queries qt), threshold, and run stage 2 on hits.
+// the tiled queries qt), threshold, and run stage 2 on hits.  resp_score is [B][models.m].
 hipError_t launch_finalize_verify(const uint64_t* part, int P, bool part_groups, const uint16_t* keys_tiled,
-                                  const uint16_t* qt, int B, int n_rows, const void* la,
-                                  int dtype, int d, const int32_t* la_tok, int k, const uint16_t* emb, int d_pad,
-                                  const int32_t* tokens, int k_cap, float tau_q, float tau_r, int32_t* idx,
-                                  float* score, float* resp_score, int32_t* decision, hipStream_t s);
+                                  const uint16_t* qt, int B, int n_rows, int dtype, int d_keys,
+                                  const PrefixModels& models, const int32_t* la_tok, int k, const int32_t* tokens,
+                                  int k_cap, float tau_q, int32_t* idx, float* score, float* resp_score,
+                                  int32_t* decision, hipStream_t s);
 
 // Most partials a stage-1 launch may write per query.
 constexpr int kMaxPartials = 1024;

@@ -39,6 +39,12 @@ CLS_MISS, CLS_BENIGN, CLS_COLLISION = 0, 1, 2
 # stream identifiers for SeedSequence spawn keys
 _S_KEYS, _S_EMB, _S_TOK, _S_CENT, _S_ASSIGN = 0, 1, 2, 3, 4
 _S_QCLASS, _S_QVEC, _S_QLOOK, _S_DUP = 10, 11, 12, 13
+_S_ENS_EMB, _S_ENS_LOOK = 20, 40       # + model index
+
+# Prefix-embedding dimensions of the lookahead ensemble the paper evaluates
+# (Section 5.4, number of lookahead checks): BGE-large, MiniLM, MPNet,
+# Qwen3-Embedding-0.6B.
+ENSEMBLE_DIMS = (1024, 384, 768, 1024)
 
 
 @dataclasses.dataclass(frozen=True)
@@ -294,6 +300,73 @@ def queries(sp: Spec, keys: np.ndarray, emb: np.ndarray, tokens: np.ndarray, dup
                 cls=cls[perm], target=expect[perm], cos=cos[perm])
 
 
+def ensemble_entries(sp: Spec, d_models, first: int, n: int, threads: int | None = None):
+    """Rows [first, first+n) of each prefix model's stored embeddings: one [n][d_i] array per model,
+    unit(N(0, I)) rows cast to the spec's input dtype."""
+    out = [np.empty((n, di), np.float32 if sp.in_dtype == F32 else np.uint16) for di in d_models]
+    c0, c1 = first // GEN_CHUNK, (first + n + GEN_CHUNK - 1) // GEN_CHUNK
+
+    def work(job):
+        i, c = job
+        r0 = c * GEN_CHUNK
+        x = _rng(sp.seed, _S_ENS_EMB + i, c).standard_normal((GEN_CHUNK, d_models[i]), dtype=np.float32)
+        lo, hi = max(r0, first), min(r0 + GEN_CHUNK, first + n)
+        out[i][lo - first:hi - first] = _cast(_unit_rows(x[lo - r0:hi - r0]), sp.in_dtype)
+
+    jobs = [(i, c) for i in range(len(d_models)) for c in range(c0, c1)]
+    if len(jobs) <= 1:
+        for j in jobs:
+            work(j)
+    else:
+        with ThreadPoolExecutor(threads or min(16, os.cpu_count() or 1)) as ex:
+            list(ex.map(work, jobs))
+    return out
+
+
+def ensemble_lookahead(sp: Spec, d_models, stored, tokens, q: dict, stream_chunk: int = 0, frac_substituted=0.5,
+                       frac_fooled=0.3):
+    """Lookahead embeddings of a query batch under each prefix model of an ensemble.
+
+    q is the dict queries() returns (its cls, target and la_tok); stored[i] holds model i's prefix
+    embeddings of every entry and tokens the entries' prefix tokens.  Per query and model the lookahead is rho * e + sqrt(1 - rho^2) * v around
+    the target entry's stored prefix e (v a random unit vector orthogonal to e): benign queries draw
+    rho ~ U[0.70, 0.98] (the benign prefix-cosine band, P10 near the 0.70 threshold, Appendix A.2);
+    collisions draw rho ~ N(0.49, 0.09) (Table 3), except that a fraction frac_fooled of them has one
+    model, chosen at random, fooled at rho ~ U[0.75, 0.95] -- the case an ensemble exists for
+    (Section 4.4).  Misses get unrelated vectors.  Benign queries carry their target's first k tokens,
+    except that a fraction frac_substituted of them has one token replaced, so that the embedding models,
+    not identical tokens, decide them.
+    Returns (list of [B][d_i] arrays, la_tok).
+    """
+    rng = _rng(sp.seed, _S_ENS_LOOK, stream_chunk)
+    cls, target = q["cls"], q["target"]
+    la_tok = np.array(q["la_tok"], np.int32, copy=True)
+    B, k = la_tok.shape
+    m = len(d_models)
+    ben = cls == CLS_BENIGN
+    col = cls == CLS_COLLISION
+    la_tok[ben] = tokens[target[ben], :k]
+    sub = ben & (rng.random(B) < frac_substituted)
+    pos = rng.integers(0, k, B)
+    bump = 1 + rng.integers(0, sp.vocab - 1, B)
+    la_tok[sub, pos[sub]] = (la_tok[sub, pos[sub]] + bump[sub]) % sp.vocab
+    fooled = np.where(col & (rng.random(B) < frac_fooled), rng.integers(0, m, B), -1)
+    out = []
+    for i, di in enumerate(d_models):
+        lrng = _rng(sp.seed, _S_ENS_LOOK + 1 + i, stream_chunk)
+        la = _unit_rows(lrng.standard_normal((B, di)))
+        planted = ben | col
+        if planted.any():
+            e = _unit_rows(as_f64(stored[i][target[planted]], sp.in_dtype))
+            rho = np.where(ben[planted], lrng.uniform(0.70, 0.98, B)[planted],
+                           np.clip(lrng.normal(0.49, 0.09, B)[planted], -0.99, 0.99))
+            hit = fooled[planted] == i
+            rho = np.where(hit, lrng.uniform(0.75, 0.95, B)[planted], rho)[:, None]
+            la[planted] = rho * e + np.sqrt(1 - rho * rho) * _orth_unit(lrng, e)
+        out.append(_cast(la, sp.in_dtype))
+    return out, la_tok
+
+
 def generate(sp: Spec | str, threads: int | None = None, **overrides) -> Workload:
     """Build the cache contents and one batch of queries for a spec."""
     if isinstance(sp, str):
@@ -311,4 +384,5 @@ def generate(sp: Spec | str, threads: int | None = None, **overrides) -> Workloa
 
 __all__ = ["Spec", "Workload", "CONFIGS", "spec", "generate", "entries", "queries", "to_bf16_bits",
            "bf16_bits_to_f64", "as_f64", "CLS_MISS", "CLS_BENIGN", "CLS_COLLISION",
-           "F32", "BF16", "GEN_CHUNK", "SERVE_SMALL_CALL_B"]
+           "F32", "BF16", "GEN_CHUNK", "SERVE_SMALL_CALL_B", "ENSEMBLE_DIMS", "ensemble_entries",
+           "ensemble_lookahead"]

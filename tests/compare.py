@@ -80,3 +80,41 @@ def compare(gpu: dict, orc: dict, keys_q, emb_q, tokens, q_q, a_q, u, tau_q, tau
     assert np.all(dr <= SCORE_TOL), f"resp_score off by {dr.max()}"
     assert np.all(np.abs(g["score"]) <= 1) and np.all(np.abs(g["resp_score"][~gn]) <= 1)
     return dict(n=len(rows), idx_exact=int(same.sum()), near_tie=int((~same).sum()), thr_margin=int(thr.sum()))
+
+
+def compare_ensemble(gpu: dict, orc: dict, s1: dict, tau_q, tau_r, rows=None) -> dict:
+    """Check an ensemble lookup (resp_score [B][m]) against oracle.lookup_ensemble on the same rows.
+
+    s1 is oracle.lookup on the same keys and queries, used only for its stage-1 s_best and margin.  Same rules
+    as compare(): idx equal unless the oracle's top-2 margin is below 2e-3 (such rows are counted and their
+    stage 2 is not compared); score within 1e-3; for rows with the oracle's entry, every model's
+    resp_score within 1e-3 with NaN in the same places, and the decision equal unless the score is within
+    2e-3 of tau_q or some model's prefix score is within 2e-3 of its threshold.
+    """
+    B = len(orc["idx"])
+    rows = np.arange(B) if rows is None else np.asarray(rows)
+    g = {n: np.asarray(gpu[n])[rows] for n in ("idx", "score", "resp_score", "decision")}
+    tau_r = np.asarray(tau_r, np.float32)
+    ds = np.abs(g["score"].astype(np.float64) - orc["score"].astype(np.float64))
+    bad = np.nonzero(~(ds <= SCORE_TOL) & ~(np.isnan(g["score"]) & np.isnan(orc["score"])))[0]
+    assert len(bad) == 0, f"score off by > {SCORE_TOL} at queries {rows[bad][:10]}: {ds[bad][:10]}"
+    same = g["idx"] == orc["idx"]
+    bad = np.nonzero(~same & ~(s1["margin"] < MARGIN))[0]
+    assert len(bad) == 0, f"idx differs at queries {rows[bad][:10]}: gpu {g['idx'][bad]} oracle {orc['idx'][bad]}"
+    gr, orr = g["resp_score"][same], orc["resp_score"][same]
+    ran = ~np.isnan(orr).any(axis=1)
+    thr = (np.abs(g["score"][same] - np.float32(tau_q)) < MARGIN) | \
+          (ran & (np.abs(orr - tau_r[None, :]) < MARGIN).any(axis=1))
+    bad = np.nonzero((g["decision"][same] != orc["decision"][same]) & ~thr)[0]
+    assert len(bad) == 0, (f"decision differs at queries {rows[same][bad][:10]}: gpu {g['decision'][same][bad][:10]}"
+                           f" oracle {orc['decision'][same][bad][:10]}")
+    gn, on = np.isnan(gr), np.isnan(orr)
+    bad = np.nonzero((gn != on).any(axis=1) & ~thr)[0]
+    assert len(bad) == 0, f"resp_score NaN-ness differs at queries {rows[same][bad][:10]}"
+    assert np.all(gn.all(axis=1) | ~gn.any(axis=1)), "stage 2 ran for some models only"
+    both = ~gn & ~on
+    dr = np.abs(gr[both].astype(np.float64) - orr[both])
+    assert dr.size == 0 or dr.max() <= SCORE_TOL, f"resp_score off by {dr.max()}"
+    assert np.all(np.abs(g["resp_score"][~np.isnan(g["resp_score"])]) <= 1)
+    return dict(n=len(rows), idx_exact=int(same.sum()), near_tie=int((~same).sum()), thr_margin=int(thr.sum()),
+                decisions=np.bincount(g["decision"], minlength=4).tolist())

@@ -14,7 +14,11 @@ LIB = os.path.join(ROOT, "paper_2608_01718_amd", "liblacache.so")
 @pytest.fixture(scope="module")
 def lib():
     if not os.path.exists(LIB):
-        from paper_2608_01718_amd import build as b
+        import importlib.util
+        spec = importlib.util.spec_from_file_location("lacache_build",
+                                                      os.path.join(ROOT, "paper_2608_01718_amd", "build.py"))
+        b = importlib.util.module_from_spec(spec)
+        spec.loader.exec_module(b)
         b.build()
     return ctypes.CDLL(LIB)
 
@@ -66,6 +70,24 @@ def test_argument_checks_before_any_device_work(lib):
     assert lib.lacache_set_small_batch(None, 16) == EINVAL
     lib.lacache_profile_read.argtypes = [P, P, P]
     assert lib.lacache_profile_read(None, None, None) == EINVAL
+    lib.lacache_create_ensemble.argtypes = [ctypes.POINTER(P), ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                                            ctypes.c_int, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, P]
+    dims = (ctypes.c_int32 * 9)(64, 32, 16, 8, 4, 2, 1, 128, 256)
+    bad_dims = (ctypes.c_int32 * 2)(64, 0)
+    huge_dims = (ctypes.c_int32 * 2)(64, 16385)
+    for m, arr in ((0, dims), (9, dims), (-1, dims), (2, None), (2, bad_dims), (2, huge_dims)):
+        assert lib.lacache_create_ensemble(ctypes.byref(h), 10, 64, 8, 1, 16, 0, m,
+                                           ctypes.cast(arr, P) if arr is not None else None) == EINVAL, m
+        assert not h.value
+    lib.lacache_models.argtypes = [P]
+    lib.lacache_models.restype = ctypes.c_int32
+    assert lib.lacache_models(None) == -1
+    lib.lacache_insert_ensemble.argtypes = [P, P, P, P, ctypes.c_int32, P, P]
+    assert lib.lacache_insert_ensemble(None, None, None, None, 0, None, None) == EINVAL
+    lib.lacache_lookup_ensemble.argtypes = [P] * 5 + [ctypes.c_float, P, ctypes.c_int32] + [P] * 5
+    assert lib.lacache_lookup_ensemble(None, None, None, None, 0, 0.5, None, 1, None, None, None, None, None) == EINVAL
+    lib.lacache_export_prefix.argtypes = [P, ctypes.c_int32, ctypes.c_int64, ctypes.c_int32, P, P]
+    assert lib.lacache_export_prefix(None, 0, 0, 0, None, None) == EINVAL
     lib.lacache_strerror.restype = ctypes.c_char_p
     assert lib.lacache_strerror(-2) == b"cache capacity exceeded"
     assert lib.lacache_strerror(12345) == b"unknown error code"
