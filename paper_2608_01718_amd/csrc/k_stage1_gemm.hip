@@ -11,20 +11,25 @@
 // contiguous range of 256-key tiles.  Each key tile is consumed in stages of
 // kBK columns of d: a stage (256 x kBK keys + 256 x kBK queries, 1 KiB chunks
 // of the tiled store layout) is copied by buffer loads straight into one of
-// kNBuf LDS buffers (no staging registers), kNBuf - 1 stages ahead of the one
-// being multiplied.  Waves are arranged 2 (key halves of 128) x 4 (query
-// quarters of 64), two per SIMD; a wave multiplies its 128 x 64 block with
+// two LDS buffers (no staging registers), one stage ahead of the one being
+// multiplied.  Waves are arranged 2 (key halves of 128) x 4 (query quarters
+// of 64), two per SIMD; a wave multiplies its 128 x 64 block with
 // v_mfma_f32_32x32x16_bf16, keys as the row operand, so a lane's 16
-// accumulators per fragment are 16 keys of one query.  The first MFMAs of a
-// key tile start from a zero accumulator.  After the last stage of a key tile
-// each lane takes, per query, the maximum of each of its four 32-row groups
-// and keeps a running (best score, 32-row group); only a strictly larger score
-// replaces the best and the lowest group wins within a tile, so ties keep the
-// lowest group.  The exact lowest row is recovered afterwards by replaying the
-// winning group (launch.hpp), which keeps this epilogue branch-free.  The one
-// partial key tile (rows beyond the entry count are zero padding and must not
-// win) is handled by a separate, masked instantiation.  At the end each
-// workgroup writes one packed candidate per query.
+// accumulators per fragment are 16 keys of one query.  Within a stage the
+// MFMAs of one 16-column substep run while the next substep's fragments are
+// read; the workgroup synchronises before the last substep's MFMAs, so the
+// copy of the stage after next and the first fragment reads of the next stage
+// are issued under matrix-core work rather than behind a drained pipeline.
+// The first MFMAs of a key tile start from a zero accumulator.  After the last
+// stage of a key tile each lane takes, per query, the maximum of each of its
+// four 32-row groups and keeps a running (best score, 32-row group); only a
+// strictly larger score replaces the best and the lowest group wins within a
+// tile, so ties keep the lowest group.  The exact lowest row is recovered
+// afterwards by replaying the winning group (launch.hpp), which keeps this
+// epilogue branch-free.  The one partial key tile (rows beyond the entry
+// count are zero padding and must not win) is handled by a separate, masked
+// instantiation.  At the end each workgroup writes one packed candidate per
+// query.
 #include <cstdlib>
 #include <type_traits>
 
@@ -41,18 +46,14 @@ constexpr int QF = 2;                                // 32-query MFMA fragments 
 #ifndef LACACHE_GEMM_BK
 #define LACACHE_GEMM_BK 64
 #endif
-#ifndef LACACHE_GEMM_NBUF
-#define LACACHE_GEMM_NBUF 2
-#endif
 constexpr int kBK = LACACHE_GEMM_BK;                 // columns of d per LDS stage (32 or 64)
-constexpr int kNBuf = LACACHE_GEMM_NBUF;             // LDS stage buffers (prefetch distance kNBuf - 1)
+constexpr int kNBuf = 2;                             // LDS stage buffers
 constexpr int kBlk = kBK / 32;                       // 32-column blocks of the tiled layout per stage
 constexpr int kSub = kBK / 16;                       // MFMA k-steps (16 columns) per stage
 constexpr int kChunks = 16 * kBlk;                   // 1 KiB chunks per operand per stage
 constexpr int kStageBytes = 2 * kChunks * 1024;      // keys + queries
 constexpr int kPerWave = kChunks / kWaves;           // chunks of each operand a wave copies per stage
-constexpr int kLoadsPerStage = 2 * kPerWave;         // buffer loads per wave per stage
-static_assert((kNBuf & (kNBuf - 1)) == 0 && kNBuf * kStageBytes <= 160 * 1024, "LDS stage ring");
+static_assert(kNBuf * kStageBytes <= 160 * 1024, "two LDS stage buffers");
 
 // byte offset, inside one operand's stage, of the 32x32x16 fragment read by lane l:
 // rows [row0, row0 + 32), columns 16 s .. 16 s + 15 of the stage (chunk j of a stage = 16-row group
@@ -74,26 +75,6 @@ __device__ inline void buffer_to_lds16(__amdgpu_buffer_rsrc_t r, uint32_t voff, 
                                        unsigned char* lds_wave_base) {
     __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds_wave_base, 16, voff,
                                              soff, 0, 0);
-}
-
-// s_waitcnt with the vector-memory count N and the other counters left free (gfx9 encoding).
-template <int N>
-__device__ inline void wait_vmcnt() {
-    static_assert(N >= 0 && N < 64, "vmcnt range");
-    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
-}
-
-// Wait until at most `stages` stages of this wave's copies are still in flight.
-__device__ inline void wait_stages_in_flight(int stages) {
-    static_assert(kNBuf <= 4, "up to three stages in flight");
-    if (stages >= 3)
-        wait_vmcnt<3 * kLoadsPerStage>();
-    else if (stages == 2)
-        wait_vmcnt<2 * kLoadsPerStage>();
-    else if (stages == 1)
-        wait_vmcnt<kLoadsPerStage>();
-    else
-        wait_vmcnt<0>();
 }
 
 }  // namespace
@@ -128,7 +109,8 @@ __global__ __launch_bounds__(512, 1) void k_stage1_gemm(const u32x4* __restrict_
     }
     const int kt0 = MASKED ? n_ktiles : (int)((int64_t)range * n_ktiles / n_ranges);
     const int kt1 = MASKED ? n_ktiles + 1 : (int)((int64_t)(range + 1) * n_ktiles / n_ranges);
-    const int T = (kt1 - kt0) * (kc / kBlk);  // stages of the whole range
+    const int spt = kc / kBlk;                // stages per key tile
+    const int T = (kt1 - kt0) * spt;          // stages of the whole range
 
     // running best of each lane per 32-query fragment b: the score, and the 32-row group (global row / 32)
     // holding it -- the exact row is recovered later by replaying that group (see launch.hpp)
@@ -140,63 +122,68 @@ __global__ __launch_bounds__(512, 1) void k_stage1_gemm(const u32x4* __restrict_
         bgrp[q] = 0x7FFFFFFF;
     }
 
-    // stages are consumed in order; stage t covers columns kBK (t % spt) .. of key tile kt0 + t / spt and is
-    // copied by buffer loads straight into LDS buffer t % kNBuf, kNBuf - 1 stages ahead.  Wave w copies
-    // chunks w, w + 8, ... of both operands, lane l moving bytes 16 l .. 16 l + 15 of a chunk.
-    const int spt = kc / kBlk;  // stages per key tile
+    // copies: stage u covers columns kBK (u % spt) .. of key tile kt0 + u / spt and goes to LDS buffer u % 2.
+    // Wave w copies chunks j = w, w + 8, ... of both operands; the buffer offset of chunk j in stage column
+    // block i_st is jb[p] + i_st * kBlk * 1024.
     const uint32_t tile_bytes = (uint32_t)kTile * kc * 64;
     const __amdgpu_buffer_rsrc_t qr = make_rsrc(qt + (int64_t)qtile * 16 * kc * 64, tile_bytes);
     const uint32_t voff = (uint32_t)lane * 16;
-    int i_kt = kt0, i_st = 0, i_buf = 0;  // next stage to copy
+    uint32_t jb[kPerWave];
+#pragma unroll
+    for (int p = 0; p < kPerWave; ++p) {
+        const int j = p * kWaves + wid;
+        jb[p] = (uint32_t)(((j / kBlk) * kc + (j % kBlk)) * 1024);
+    }
+    const u32x4* kbase = keys + (int64_t)kt0 * 16 * kc * 64;  // key tile of the next copy
+    int i_st = 0, i_buf = 0;
     auto issue = [&]() {
-        const __amdgpu_buffer_rsrc_t kr = make_rsrc(keys + (int64_t)i_kt * 16 * kc * 64, tile_bytes);
+        const __amdgpu_buffer_rsrc_t kr = make_rsrc(kbase, tile_bytes);
         unsigned char* dk = lds + i_buf * kStageBytes;
         unsigned char* dq = dk + kChunks * 1024;
+        const uint32_t so = (uint32_t)i_st * (kBlk * 1024);
 #pragma unroll
         for (int p = 0; p < kPerWave; ++p) {
             const int j = p * kWaves + wid;
-            const uint32_t soff = (uint32_t)((((j / kBlk) * kc) + i_st * kBlk + (j % kBlk)) * 1024);
-            buffer_to_lds16(kr, voff, soff, dk + j * 1024);
-            buffer_to_lds16(qr, voff, soff, dq + j * 1024);
+            buffer_to_lds16(kr, voff, jb[p] + so, dk + j * 1024);
+            buffer_to_lds16(qr, voff, jb[p] + so, dq + j * 1024);
         }
-        i_buf = (i_buf + 1) & (kNBuf - 1);
+        i_buf ^= 1;
         if (++i_st == spt) {
             i_st = 0;
-            ++i_kt;
+            kbase += 16 * kc * 64;
         }
+    };
+    // fragments of substep s of the stage in LDS buffer `buf`
+    auto read_frags = [&](int buf, int s, u32x4* fa, u32x4* fb) {
+        const unsigned char* sk = lds + buf * kStageBytes;
+        const unsigned char* sq = sk + kChunks * 1024;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) fa[i] = *(const u32x4*)(sk + frag_offset(wk * 128 + i * 32, s, lane));
+#pragma unroll
+        for (int i = 0; i < QF; ++i) fb[i] = *(const u32x4*)(sq + frag_offset(wq * 64 + i * 32, s, lane));
     };
 
     f32x16 acc[4][QF];
+    u32x4 fa[kSub][4], fb[kSub][QF];
     int kt = kt0, st = 0;
-    // one stage: multiply LDS buffer t % kNBuf.  FIRST: the stage opens a key tile, so its first MFMAs
-    // start from a zero accumulator.
+
+    // Stage t (buffer t % 2), fragments of its substep 0 already in fa[0] / fb[0].  Substeps 0 .. kSub-2 are
+    // multiplied while the fragments of the next substep are read; then the workgroup synchronises (stage
+    // t + 1 has landed, every wave is done reading buffer t % 2), the copy of stage t + 2 into buffer t % 2
+    // and the reads of stage t + 1's first fragments are issued, and the last substep's MFMAs run over
+    // their latency.  FIRST: stage t opens a key tile, its first MFMAs start from a zero accumulator.
     auto step = [&](int t, auto first_tag) {
         constexpr bool FIRST = decltype(first_tag)::value;
-        // buffer (t + kNBuf - 1) % kNBuf was last read in stage t - 1, which ended with a barrier
-        if (t + kNBuf - 1 < T) issue();
-        const unsigned char* sk = lds + (t & (kNBuf - 1)) * kStageBytes;
-        const unsigned char* sq = sk + kChunks * 1024;
-        u32x4 fa[kSub][4], fb[kSub][QF];
+        const int buf = t & 1;
 #pragma unroll
-        for (int s = 0; s < kSub; ++s) {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) fa[s][i] = *(const u32x4*)(sk + frag_offset(wk * 128 + i * 32, s, lane));
-#pragma unroll
-            for (int i = 0; i < QF; ++i) fb[s][i] = *(const u32x4*)(sq + frag_offset(wq * 64 + i * 32, s, lane));
-        }
-#pragma unroll
-        for (int s = 0; s < kSub; ++s)
+        for (int s = 0; s + 1 < kSub; ++s) {
+            read_frags(buf, s + 1, fa[s + 1], fb[s + 1]);
 #pragma unroll
             for (int a = 0; a < 4; ++a)
 #pragma unroll
                 for (int b = 0; b < QF; ++b)
                     acc[a][b] = mfma32x32x16(fa[s][a], fb[s][b], (FIRST && s == 0) ? f32x16{} : acc[a][b]);
-        // instruction order: the fragment reads of substep 0, then each substep's MFMAs interleaved one to
-        // one with the next substep's fragment reads, so LDS latency hides behind matrix-core work
-        constexpr int kReads = 4 + QF, kMfma = 4 * QF;
-        __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);  // DS reads
-#pragma unroll
-        for (int s = 1; s < kSub; ++s) {
+            constexpr int kReads = 4 + QF, kMfma = 4 * QF;
 #pragma unroll
             for (int i = 0; i < kReads; ++i) {
                 __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
@@ -204,7 +191,22 @@ __global__ __launch_bounds__(512, 1) void k_stage1_gemm(const u32x4* __restrict_
             }
             __builtin_amdgcn_sched_group_barrier(0x008, kMfma - kReads, 0);
         }
-        __builtin_amdgcn_sched_group_barrier(0x008, kMfma, 0);
+        // every fragment read of buffer t % 2 has returned before any wave may overwrite that buffer
+        __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+        __syncthreads();
+        if (t + 2 < T) issue();
+        u32x4 na[4], nb[QF];
+        if (t + 1 < T) read_frags(buf ^ 1, 0, na, nb);
+        constexpr int L = kSub - 1;
+#pragma unroll
+        for (int a = 0; a < 4; ++a)
+#pragma unroll
+            for (int b = 0; b < QF; ++b)
+                acc[a][b] = mfma32x32x16(fa[L][a], fb[L][b], (FIRST && L == 0) ? f32x16{} : acc[a][b]);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) fa[0][i] = na[i];
+#pragma unroll
+        for (int i = 0; i < QF; ++i) fb[0][i] = nb[i];
 
         if (++st == spt) {
             // end of key tile kt: lane holds, for query column wq*64 + b*32 + lane%32, the keys
@@ -235,22 +237,21 @@ __global__ __launch_bounds__(512, 1) void k_stage1_gemm(const u32x4* __restrict_
             st = 0;
             ++kt;
         }
-        // stage t + 1 must have landed (for every wave) before the next stage reads it
-        const int last_issued = (t + kNBuf - 1 < T) ? t + kNBuf - 1 : T - 1;
-        const int after = last_issued - (t + 1);
-        wait_stages_in_flight(after < 0 ? 0 : after);
-        __syncthreads();
     };
 
-    for (int t = 0; t < kNBuf - 1 && t < T; ++t) issue();
-    wait_stages_in_flight((T < kNBuf - 1 ? T : kNBuf - 1) - 1);
-    __syncthreads();
+    if (T > 0) {
+        issue();
+        __syncthreads();
+        if (T > 1) issue();
+        read_frags(0, 0, fa[0], fb[0]);
+    }
     for (int t = 0; t < T; ++t) {
         if (st == 0)
             step(t, std::true_type{});
         else
             step(t, std::false_type{});
     }
+    __syncthreads();
 
     // merge lanes l and l^32 (same query), then the two key-half waves, and write one candidate per query
     uint64_t* red = (uint64_t*)lds;  // [2 key halves][256 queries]; the stage buffers are no longer read
