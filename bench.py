@@ -15,7 +15,10 @@ same keys with the four-model lookahead ensemble (Section 4.4) under
 each, "roofline" rates the stage-1 kernel, timed with HIP events recorded by
 the library on the launch stream, against the MI355X peak (bf16 dense MFMA
 2.5 PFLOP/s, HBM 8 TB/s).  "cpu_baseline" times the CPU oracle on a bounded
-sample of the same workload on the host cores.
+sample of the same workload on the host cores.  "attainable" rates the same
+kernels against what this GPU sustains, measured at start-up by the
+roofline_probe executable built beside the library: v_mfma_f32_32x32x16_bf16
+throughput on random bf16 operands, and a plain streaming read.
 """
 from __future__ import annotations
 
@@ -43,6 +46,8 @@ def parse():
     ap.add_argument("--no-secondary", action="store_true", help="measure only the headline workload")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
     ap.add_argument("--no-ensemble", action="store_true", help="skip the lookahead-ensemble measurement")
+    ap.add_argument("--no-probe", action="store_true",
+                    help="skip the attainable-ceiling probe (sustained MFMA rate on random bf16, HBM streaming read)")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="per-launch HBM traffic measured with rocprofv3 counters (JSON), if present")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
@@ -112,6 +117,20 @@ def pmc_summary(root, out_path, copy_mib):
                      "write_bytes": write, "traffic_bytes": fetch + write, "dispatches": len(fv)}
     json.dump(out, open(out_path, "w"), indent=1)
     print(json.dumps(out), flush=True)
+
+
+def attainable_ceilings():
+    """Run the roofline probe executable built beside the library (a child process) and return its JSON."""
+    import subprocess
+    exe = os.path.join(ROOT, "paper_2608_01718_amd", "roofline_probe")
+    if not os.path.exists(exe):
+        log("[bench] roofline_probe not built; attainable ceilings not reported")
+        return None
+    r = subprocess.run([exe], capture_output=True, text=True, timeout=120)
+    if r.returncode != 0:
+        log(f"[bench] roofline_probe failed ({r.returncode}): {r.stderr.strip()}")
+        return None
+    return json.loads(r.stdout.strip().splitlines()[-1])
 
 
 def log(*a):
@@ -282,6 +301,7 @@ def main():
     if args.calibrate_copy_mib:
         calibrate_copy(args.calibrate_copy_mib)
         return
+    probe = None if args.no_probe else attainable_ceilings()
     import torch
     import synth
     import paper_2608_01718_amd as lc  # raises if liblacache.so has not been built
@@ -326,6 +346,18 @@ def main():
             "stage1_kernel_avg_ms": secondary["roofline"]["kernel_avg_ms"], "rates": secondary["rates"]}
     if ensemble:
         line["ensemble"] = ensemble
+    if probe:
+        # the same kernels rated against what this GPU sustains: MFMA throughput on random bf16 operands
+        # (operand-dependent power lowers the clock below the datasheet's) and a plain streaming read
+        att = {"mfma_bf16_random_tflops": probe["mfma_random_tflops"],
+               "mfma_bf16_constant_tflops": probe["mfma_constant_tflops"], "hbm_read_gbs": probe["hbm_read_gbs"]}
+        for key, res in (("frac", main_res), ("secondary_frac", secondary)):
+            if not res:
+                continue
+            rf = res["roofline"]
+            ceil = probe["mfma_random_tflops"] if rf["bound"] == "mfma" else probe["hbm_read_gbs"]
+            att[key] = rf["achieved"] / ceil
+        line["attainable"] = att
     print(json.dumps(line), flush=True)
 
 

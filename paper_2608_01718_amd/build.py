@@ -39,10 +39,27 @@ def _compile(src: str) -> str:
     return obj
 
 
+PROBE_SRC = "roofline_probe.hip"
+PROBE = os.path.join(HERE, "roofline_probe")
+
+
+def _build_probe() -> str:
+    """The attainable-ceiling probe bench.py reports beside the datasheet peaks (a separate executable)."""
+    obj = _compile(PROBE_SRC)
+    tmp = PROBE + ".tmp"
+    r = subprocess.run([HIPCC, f"--offload-arch={ARCH}", "-o", tmp, obj], capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"link of {PROBE_SRC} failed:\n{r.stderr}")
+    os.replace(tmp, PROBE)
+    return PROBE
+
+
 def build() -> str:
     os.makedirs(BUILD_DIR, exist_ok=True)
-    with ThreadPoolExecutor(min(8, len(SOURCES))) as ex:
+    with ThreadPoolExecutor(min(8, len(SOURCES) + 1)) as ex:
+        probe = ex.submit(_build_probe)
         objs = list(ex.map(_compile, SOURCES))
+        probe.result()
     tmp = OUT + ".tmp"
     r = subprocess.run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs],
                        capture_output=True, text=True)
