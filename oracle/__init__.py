@@ -11,7 +11,9 @@ What it computes, and the passages it follows, is stated in the header of
 lowest index on ties, hit when the clamped score >= tau_q (Algorithm 1,
 Section 5.1); for hits only, the lookahead check on the matched entry --
 identical first-k tokens, or prefix-embedding cosine >= tau_r (Algorithm 1,
-Section 4.2 cache structure, Section 5.1).
+Section 4.2 cache structure, Section 5.1); with m lookahead models, all m
+checks (Section 4.4); thresholds from benign pairs as capped percentiles of
+their cosines (Appendix A.2).
 """
 from __future__ import annotations
 
@@ -58,6 +60,9 @@ def lib():
         L.lco_lookup.argtypes = [P, P, P, i64, i32, i32, P, P, P, i32, f32, f32, i32, P, P, P, P, P, P]
         L.lco_decide.argtypes = [P, P, P, i64, i32, i32, P, P, P, i32, f32, f32, i32, P, P, P, P, P]
         L.lco_first_identical.argtypes = [P, i64, i32, i64]
+        f64 = ctypes.c_double
+        L.lco_threshold_rule.argtypes = [P, i64, f64, f64, P, P]
+        L.lco_calibrate.argtypes = [P, P, i64, i32, f64, f64, P, P, P]
         L.lco_first_identical.restype = i64
         L.lco_num_threads.restype = ctypes.c_int
         L.lco_lookup_ensemble.argtypes = [P, i64, i32, P, i32, f32, i32, P, P, P, P, P, i32, P, i32, P, P, P, P]
@@ -176,6 +181,29 @@ def lookup_ensemble(keys_q, q_q, tau_q: float, embs_q, as_q, tau_r, tokens, u, k
                               tokens.shape[1], _ptr(u), k, _ptr(out["idx"]), _ptr(out["score"]),
                               _ptr(out["resp_score"]), _ptr(out["decision"]))
     return out
+
+
+def threshold_rule(sims, p: float, cap: float):
+    """Appendix A.2 rule on given similarities: (P_p with linear interpolation, min(cap, P_p))."""
+    x = np.ascontiguousarray(sims, np.float64).ravel()
+    assert x.size >= 1 and 0.0 <= p <= 100.0
+    P, tau = ctypes.c_double(), ctypes.c_double()
+    lib().lco_threshold_rule(_ptr(x), x.size, float(p), float(cap), ctypes.byref(P), ctypes.byref(tau))
+    return P.value, tau.value
+
+
+def calibrate(a_q, b_q, p: float, cap: float) -> dict:
+    """Threshold calibration over pairs of quantised vectors a_q[j], b_q[j] ([n][d] bf16 bits).
+    Returns sims (float64 [n], clamped cosines), P (the percentile) and tau = min(cap, P)."""
+    a_q = _c(a_q, np.uint16)
+    b_q = _c(b_q, np.uint16)
+    assert a_q.shape == b_q.shape and a_q.ndim == 2 and a_q.shape[0] >= 1
+    n, d = a_q.shape
+    sims = np.empty(n, np.float64)
+    P, tau = ctypes.c_double(), ctypes.c_double()
+    lib().lco_calibrate(_ptr(a_q), _ptr(b_q), n, d, float(p), float(cap), _ptr(sims), ctypes.byref(P),
+                        ctypes.byref(tau))
+    return dict(sims=sims, P=P.value, tau=tau.value)
 
 
 def num_threads() -> int:

@@ -27,11 +27,15 @@
  *             agrees) or when the prefix-embedding cosine is >= tau_r
  *             (Section 5.1, lookahead check sim(f_k(x), f_k(x')) >= tau_a).
  *
+ *   calibrate Thresholds from benign pairs (Appendix A.2): the p-th percentile
+ *             of the pair cosines, capped from above.
+ *
  * Decision codes: 0 MISS, 1 REJECT (collision detected), 2 HIT, 3 HIT_EXACT.
  */
 #include <math.h>
 #include <omp.h>
 #include <stdint.h>
+#include <stdlib.h>
 #include <string.h>
 
 #define LCO_MISS 0
@@ -331,4 +335,55 @@ void lco_lookup_ensemble(const uint16_t *keys, int64_t N, int32_t d, const uint1
                 tok_eq = 0;
         decision[b] = tok_eq ? LCO_HIT_EXACT : (all_pass ? LCO_HIT : LCO_REJECT);
     }
+}
+
+/*
+ * Threshold calibration (Appendix A.2): a threshold is the p-th percentile of
+ * the cosine similarities of benign pairs, capped from above --
+ * tau_c = min(0.80, P5) over paraphrase-pair query cosines, tau_a = min(0.70,
+ * P10) over their response-prefix cosines.  The paper does not say how a
+ * percentile between two order statistics is formed; this uses linear
+ * interpolation between the closest ranks (h = (n - 1) p / 100, the default
+ * of numpy.percentile).
+ *
+ * lco_threshold_rule: sims[0..n-1] (any order; a sorted copy is made),
+ * n >= 1, 0 <= p <= 100.  *P_out receives the percentile, *tau_out min(cap, P).
+ */
+static int cmp_double_asc(const void *x, const void *y)
+{
+    double a = *(const double *)x, b = *(const double *)y;
+    return (a > b) - (a < b);
+}
+
+void lco_threshold_rule(const double *sims, int64_t n, double p, double cap, double *P_out, double *tau_out)
+{
+    double *x = (double *)malloc((size_t)n * sizeof(double));
+    memcpy(x, sims, (size_t)n * sizeof(double));
+    qsort(x, (size_t)n, sizeof(double), cmp_double_asc);
+    double h = (double)(n - 1) * (p / 100.0);
+    int64_t lo = (int64_t)floor(h);
+    double P;
+    if (lo >= n - 1)
+        P = x[n - 1];
+    else
+        P = x[lo] + (h - (double)lo) * (x[lo + 1] - x[lo]);
+    free(x);
+    *P_out = P;
+    *tau_out = fmin(cap, P);
+}
+
+/*
+ * The calibration over n pairs of quantised vectors a[j], b[j] ([n][d]): the
+ * pair similarity is the cosine the lookup uses (dot product of the
+ * normalised, bfloat16-rounded vectors, clamped to [-1, 1]), then the rule above.
+ */
+void lco_calibrate(const uint16_t *a, const uint16_t *b, int64_t n, int32_t d, double p, double cap,
+                   double *sims, double *P_out, double *tau_out)
+{
+#pragma omp parallel for schedule(static)
+    for (int64_t j = 0; j < n; ++j) {
+        double s = lco_dot(a + j * (int64_t)d, b + j * (int64_t)d, d);
+        sims[j] = s > 1.0 ? 1.0 : (s < -1.0 ? -1.0 : s);
+    }
+    lco_threshold_rule(sims, n, p, cap, P_out, tau_out);
 }

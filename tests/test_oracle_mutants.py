@@ -34,6 +34,12 @@ MUTANTS = {
     "ensemble needs the embeddings even for identical tokens": (
         "decision[b] = tok_eq ? LCO_HIT_EXACT : (all_pass ? LCO_HIT : LCO_REJECT);",
         "decision[b] = all_pass ? (tok_eq ? LCO_HIT_EXACT : LCO_HIT) : LCO_REJECT;"),
+    "percentile position uses n instead of n - 1": ("double h = (double)(n - 1) * (p / 100.0);",
+                                                    "double h = (double)n * (p / 100.0);"),
+    "percentile takes the upper rank without interpolating": (
+        "P = x[lo] + (h - (double)lo) * (x[lo + 1] - x[lo]);", "P = x[lo + 1];"),
+    "cap applied as a floor": ("*tau_out = fmin(cap, P);", "*tau_out = fmax(cap, P);"),
+    "similarities sorted descending": ("return (a > b) - (a < b);", "return (a < b) - (a > b);"),
 }
 
 

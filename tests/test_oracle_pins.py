@@ -490,3 +490,72 @@ def test_ensemble_monotone_and_order_free():
     two = oracle.lookup_ensemble(keys, q, 0.4, embs[:2], las[:2], taus[:2], tokens, u, 4)
     loose = oracle.lookup_ensemble(keys, q, 0.4, embs[:3], las[:3], taus[:2] + [-1.0], tokens, u, 4)
     np.testing.assert_array_equal(two["decision"], loose["decision"])
+
+
+# --------------------------------------------------------------------------- threshold calibration (Appendix A.2)
+
+
+def _pairs(rng, n, d):
+    a = rng.standard_normal((n, d)).astype(np.float32)
+    # a spread of pair cosines: b = a + noise of a random scale per pair
+    scale = rng.uniform(0.05, 3.0, (n, 1)).astype(np.float32)
+    b = a + scale * rng.standard_normal((n, d)).astype(np.float32)
+    return oracle.quantise(a, oracle.F32), oracle.quantise(b, oracle.F32)
+
+
+@pytest.mark.parametrize("n,d", [(1, 16), (2, 16), (7, 40), (500, 384), (1001, 64)])
+def test_calibration_matches_numpy_percentile(n, d):
+    """The pair cosines are dot products of the quantised vectors; the percentile is numpy's default
+    (linear between closest ranks); the threshold is min(cap, percentile)."""
+    rng = np.random.default_rng(41 + n)
+    a, b = _pairs(rng, n, d)
+    sims = np.clip(np.einsum("nd,nd->n", bf.widen(a), bf.widen(b)), -1.0, 1.0)
+    for p in (0.0, 5.0, 10.0, 37.5, 50.0, 90.0, 99.0, 100.0):
+        for cap in (0.8, 0.3, 2.0):
+            o = oracle.calibrate(a, b, p, cap)
+            np.testing.assert_allclose(o["sims"], sims, rtol=0, atol=1e-12)
+            want = float(np.percentile(sims, p))
+            assert abs(o["P"] - want) <= 1e-12, (p, o["P"], want)
+            assert o["tau"] == min(cap, o["P"])
+
+
+def test_calibration_closed_forms():
+    rng = np.random.default_rng(44)
+    x = rng.uniform(-1, 1, 11)
+    s = np.sort(x)
+    assert oracle.threshold_rule(x, 0.0, 9.0)[0] == s[0]
+    assert oracle.threshold_rule(x, 100.0, 9.0)[0] == s[-1]
+    assert oracle.threshold_rule(x, 50.0, 9.0)[0] == s[5]            # h = 5 exactly
+    assert oracle.threshold_rule(x, 10.0, 9.0)[0] == s[1]            # h = 1 exactly
+    h = 10 * 0.25
+    assert abs(oracle.threshold_rule(x, 25.0, 9.0)[0] - (s[2] + (h - 2) * (s[3] - s[2]))) <= 1e-15
+    for p in (0.0, 33.0, 100.0):
+        assert oracle.threshold_rule([0.42], p, 9.0)[0] == 0.42     # one pair: every percentile is it
+    assert oracle.threshold_rule(x, 50.0, -5.0)[1] == -5.0           # the cap binds
+    # monotone in p, and order-free
+    ps = np.linspace(0, 100, 41)
+    vals = [oracle.threshold_rule(x, p, 9.0)[0] for p in ps]
+    assert all(v1 <= v2 for v1, v2 in zip(vals, vals[1:]))
+    assert oracle.threshold_rule(x[::-1], 37.0, 9.0) == oracle.threshold_rule(x, 37.0, 9.0)
+    # identical pairs have cosine 1 (up to the bf16 rounding of the normalised vector)
+    a, _ = _pairs(rng, 5, 64)
+    o = oracle.calibrate(a, a, 50.0, 2.0)
+    assert np.all(np.abs(o["sims"] - 1.0) <= 64 * 2.0 ** -8)
+
+
+def test_calibration_reproduces_the_paper_table():
+    """Appendix A.2 prints the natural percentiles and the thresholds used: tau_c = min(0.80, P5) for BGE
+    and MiniLM, tau_a = min(0.70, P10) for four (LLM, embedding) pairs.  A similarity set whose percentile
+    sits exactly on an order statistic (n = 21 for P5, n = 11 for P10: h = 1) must give the printed
+    threshold."""
+    import json
+    import os
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "paper_thresholds.json")))
+    rng = np.random.default_rng(45)
+    for table, p, n, key in (("tau_c", 5.0, 21, "P5"), ("tau_a", 10.0, 11, "P10")):
+        for name, row in g[table].items():
+            x = np.concatenate([[row[key]], rng.uniform(row[key] + 1e-3, 1.0, n - 2), [-0.5]])
+            rng.shuffle(x)
+            P, tau = oracle.threshold_rule(x, p, row["cap"])
+            assert P == row[key], (name, P)
+            assert abs(tau - row["used"]) <= 1e-12, (name, tau, row["used"])
