@@ -11,7 +11,8 @@ The headline workload (`value`) is serve_large: 4096 queries per call (the
 matrix-core-bound regime); serve_small (16 queries per call, the HBM-bound
 regime) is measured in the same run and reported under "secondary", and the
 same keys with the four-model lookahead ensemble (Section 4.4) under
-"ensemble".  For
+"ensemble", and threshold calibration over a million benign pairs
+(Appendix A.2) under "calibration".  For
 each, "roofline" rates the stage-1 kernel, timed with HIP events recorded by
 the library on the launch stream, against the MI355X peak (bf16 dense MFMA
 2.5 PFLOP/s, HBM 8 TB/s).  "cpu_baseline" times the CPU oracle on a bounded
@@ -46,6 +47,7 @@ def parse():
     ap.add_argument("--no-secondary", action="store_true", help="measure only the headline workload")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
     ap.add_argument("--no-ensemble", action="store_true", help="skip the lookahead-ensemble measurement")
+    ap.add_argument("--no-calibration", action="store_true", help="skip the threshold-calibration measurement")
     ap.add_argument("--no-probe", action="store_true",
                     help="skip the attainable-ceiling probe (sustained MFMA rate on random bf16, HBM streaming read)")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
@@ -269,6 +271,40 @@ def run_ensemble(steps, warmup, lc, torch, synth):
     return res
 
 
+def run_calibration(steps, warmup, lc, torch, synth):
+    """Threshold calibration (Appendix A.2) over a million benign pairs at d = 1024 (BGE's dimension):
+    pair cosines as the lookup computes them, then tau_c = min(0.80, P5).  One step is one
+    lacache_calibrate call; the pair-cosine pass reads 2 * n * d * 2 bytes."""
+    from tests.gpu_util import to_dev
+    n, d = 1_000_000, 1024
+    t0 = time.time()
+    a, b = synth.calibration_pairs(n, d, 0.80, 0.99, seed=66)
+    log(f"[bench] calibration: generated in {time.time() - t0:.1f}s")
+    c = lc.LaCache(16, d, 4, synth.BF16, 16, 0)
+    ad, bd = to_dev(a), to_dev(b)
+    del a, b
+    dev = torch.device("cuda", 0)
+    out = (torch.empty(n, dtype=torch.float32, device=dev), torch.empty(2, dtype=torch.float32, device=dev))
+    for _ in range(warmup):
+        c.calibrate(ad, bd, 5.0, 0.80, out=out)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        c.calibrate(ad, bd, 5.0, 0.80, out=out)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    tau = out[1].cpu().numpy()
+    c.close()
+    del ad, bd, out
+    torch.cuda.empty_cache()
+    pair_bytes = 2.0 * n * d * 2
+    return dict(workload=f"{n:,} benign pairs, d = {d} bf16, cosines in U[0.80, 0.99], tau_c = min(0.80, P5)",
+                value=n / (ms * 1e-3), unit="pairs/s", ms_per_step=ms, P5=float(tau[0]), tau=float(tau[1]),
+                pair_read_gbs=pair_bytes / (ms * 1e-3) / 1e9)
+
+
 def cpu_baseline(sp, w, call_b):
     """The CPU oracle, as it is, on a bounded sample: a few queries against the full cache."""
     import oracle
@@ -317,6 +353,7 @@ def main():
         secondary = run_workload(other, args.steps, args.warmup, lc, torch, synth, traffic_db, False)
 
     ensemble = None if args.no_ensemble else run_ensemble(args.steps, args.warmup, lc, torch, synth)
+    calibration = None if args.no_calibration else run_calibration(args.steps, args.warmup, lc, torch, synth)
 
     line = {
         "metric": "cache lookups/sec (2-stage) at N=1M,d=768; % HBM / MFMA roofline",
@@ -346,6 +383,8 @@ def main():
             "stage1_kernel_avg_ms": secondary["roofline"]["kernel_avg_ms"], "rates": secondary["rates"]}
     if ensemble:
         line["ensemble"] = ensemble
+    if calibration:
+        line["calibration"] = calibration
     if probe:
         # the same kernels rated against what this GPU sustains: MFMA throughput on random bf16 operands
         # (operand-dependent power lowers the clock below the datasheet's) and a plain streaming read

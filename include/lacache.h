@@ -185,6 +185,26 @@ int lacache_export(lacache_t h, int64_t first, int32_t n, uint16_t *keys_bf16, u
 int lacache_export_prefix(lacache_t h, int32_t model, int64_t first, int32_t n, uint16_t *emb_bf16, void *stream);
 
 /*
+ * Threshold calibration from benign pairs (Appendix A.2: tau_c = min(0.80, P5)
+ * over the cosines of benign paraphrase pairs, tau_a = min(0.70, P10) over the
+ * cosines of their response prefixes).
+ *   which       -1: the pairs are key-model vectors (dimension d);
+ *               0 <= which < m: vectors of prefix model `which` (d_resp[which])
+ *   a, b        [n][dim] (cache dtype): pair j is (a[j], b[j]); n >= 1
+ *   percentile  0 .. 100; the percentile is linear between the closest ranks,
+ *               h = (n - 1) * percentile / 100, from the order statistics
+ *               floor(h) and floor(h) + 1 (computed in double)
+ *   cap         finite upper cap of the threshold
+ * Outputs (device): sims [n] float, the pair cosines exactly as the lookup
+ * computes similarities (normalised, bfloat16-rounded vectors, float32 sums,
+ * clamped to [-1, 1]); tau [2] float: tau[0] = the percentile of sims,
+ * tau[1] = min(cap, tau[0]).  Uses the handle's calibration scratch, so
+ * calls on one handle must be ordered on one stream.
+ */
+int lacache_calibrate(lacache_t h, int32_t which, const void *a, const void *b, int64_t n, float percentile,
+                      float cap, float *sims, float *tau, void *stream);
+
+/*
  * Batch-size crossover of stage 1: batches of at most b_small queries use the
  * bandwidth-bound streaming kernel, larger ones the matrix-core GEMM kernel.
  * 0 <= b_small <= 64 (default 64; 0 sends every batch to the GEMM kernel).

@@ -36,6 +36,7 @@ _lib.lacache_insert_ensemble.argtypes = [_P, _P, ctypes.POINTER(_P), _P, _i32, c
 _lib.lacache_lookup_ensemble.argtypes = [_P, _P, ctypes.POINTER(_P), _P, _i32, _f32, ctypes.POINTER(_f32), _i32,
                                          _P, _P, _P, _P, _P]
 _lib.lacache_export_prefix.argtypes = [_P, _i32, _i64, _i32, _P, _P]
+_lib.lacache_calibrate.argtypes = [_P, _i32, _P, _P, _i64, _f32, _f32, _P, _P, _P]
 _lib.lacache_destroy.argtypes = [_P]
 _lib.lacache_insert.argtypes = [_P, _P, _P, _P, _i32, ctypes.POINTER(_i64), _P]
 _lib.lacache_lookup.argtypes = [_P, _P, _P, _P, _i32, _f32, _f32, _i32, _P, _P, _P, _P, _P]
@@ -50,8 +51,8 @@ _lib.lacache_strerror.restype = ctypes.c_char_p
 
 EXPORTED = ("lacache_create", "lacache_create_ensemble", "lacache_models", "lacache_destroy", "lacache_insert",
             "lacache_insert_ensemble", "lacache_lookup", "lacache_lookup_ensemble", "lacache_size",
-            "lacache_export", "lacache_export_prefix", "lacache_set_small_batch", "lacache_profile",
-            "lacache_profile_read", "lacache_strerror")
+            "lacache_export", "lacache_export_prefix", "lacache_calibrate", "lacache_set_small_batch",
+            "lacache_profile", "lacache_profile_read", "lacache_strerror")
 
 
 class LaCacheError(RuntimeError):
@@ -141,6 +142,9 @@ class LaCache:
 
     def export_prefix(self, model: int, first: int, n: int, stream=None):
         return lacache_export_prefix(self, model, first, n, stream)
+
+    def calibrate(self, a, b, percentile: float, cap: float, which: int = -1, out=None, stream=None):
+        return lacache_calibrate(self, which, a, b, percentile, cap, out, stream)
 
     def size(self) -> int:
         return lacache_size(self)
@@ -280,6 +284,26 @@ def lacache_export_prefix(c: LaCache, model: int, first: int, n: int, stream=Non
     _check(_lib.lacache_export_prefix(c.handle, model, first, n, emb.data_ptr(), _stream(c.device, stream)),
            "lacache_export_prefix")
     return emb
+
+
+def lacache_calibrate(c: LaCache, which: int, a, b, percentile: float, cap: float, out=None, stream=None):
+    """Pair cosines and the capped percentile threshold (Appendix A.2).  which = -1: key-model vectors of
+    dimension d; else prefix model `which`.  Returns (sims f32 [n], tau f32 [2] = (percentile, min(cap, .)))
+    on the cache's device."""
+    # an out-of-range `which` is passed through for the library to reject
+    dim = c.d_resp[which] if 0 <= which < c.m else (c.d if which == -1 else a.shape[1])
+    n = a.shape[0]
+    dev = torch.device("cuda", c.device)
+    if out is None:
+        out = (torch.empty(n, dtype=torch.float32, device=dev), torch.empty(2, dtype=torch.float32, device=dev))
+    sims, tau = out
+    for t, k, nm in ((sims, n, "sims"), (tau, 2, "tau")):
+        if t.dtype != torch.float32 or t.device != dev or t.numel() != k or not t.is_contiguous():
+            raise ValueError(f"{nm}: expected a contiguous float32 tensor of {k} elements on {dev}")
+    _check(_lib.lacache_calibrate(c.handle, int(which), _vec(a, c.in_dtype, n, dim, c.device, "a"),
+                                  _vec(b, c.in_dtype, n, dim, c.device, "b"), n, float(percentile), float(cap),
+                                  sims.data_ptr(), tau.data_ptr(), _stream(c.device, stream)), "lacache_calibrate")
+    return out
 
 
 def lacache_set_small_batch(c: LaCache, b_small: int) -> None:

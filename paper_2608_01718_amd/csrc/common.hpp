@@ -59,6 +59,30 @@ __device__ inline double load_in(const void* row, int dtype, int j) {
     return (double)bf16_to_f32(((const uint16_t*)row)[j]);
 }
 
+// Elements j0 .. j0+7 of a row as doubles (0 beyond d): one or two 16-byte loads when the chunk is whole
+// and 16-byte aligned, element loads otherwise.  The values are the same either way.
+__device__ inline void load8(const void* row, int dtype, int d, int j0, double v[8]) {
+    const size_t esz = dtype == 0 ? 4 : 2;
+    const char* p = (const char*)row + (size_t)j0 * esz;
+    if (j0 + 8 <= d && ((uintptr_t)p & 15) == 0) {
+        if (dtype == 0) {
+            const float4 x = ((const float4*)p)[0], y = ((const float4*)p)[1];
+            v[0] = x.x, v[1] = x.y, v[2] = x.z, v[3] = x.w, v[4] = y.x, v[5] = y.y, v[6] = y.z, v[7] = y.w;
+        } else {
+            const uint4 x = *(const uint4*)p;
+            const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                v[2 * t] = (double)__uint_as_float(w[t] << 16);
+                v[2 * t + 1] = (double)__uint_as_float(w[t] & 0xFFFF0000u);
+            }
+        }
+        return;
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = (j0 + e < d) ? load_in(row, dtype, j0 + e) : 0.0;
+}
+
 // ---------------------------------------------------------------------------
 // Wave-wide butterfly reductions: every lane ends with the same value, and
 // the combination order is fixed, so results are run-to-run identical.
@@ -87,41 +111,60 @@ __device__ inline uint64_t wave_max_u64(uint64_t x) {
 // bfloat16.  A zero row (or live == false) gives zeros, as do the columns
 // d .. d_pad-1.  Lane l produces columns 8l + 512t .. 8l + 512t + 7 and hands
 // them, packed, to emit(j0, u32x4).  Every kernel that quantises a vector
-// (insert, query staging, lookahead check) goes through this routine, so equal
-// inputs quantise to identical bits wherever they are stored.
+// (insert, query staging, lookahead check, calibration pairs) goes through
+// row_norm and quantise8, so equal inputs quantise to identical bits wherever
+// they are stored or compared.
 // ---------------------------------------------------------------------------
-template <class Emit>
-__device__ inline void normalise_row(const void* row, int dtype, int d, int d_pad, bool live, int lane, Emit emit) {
+__device__ inline double row_norm(const void* row, int dtype, int d, bool live, int lane) {
     double ss = 0.0;
     if (live) {
         for (int j0 = lane * 8; j0 < d; j0 += 512) {
+            double v[8];
+            load8(row, dtype, d, j0, v);
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const int j = j0 + e;
-                if (j < d) {
-                    const double v = load_in(row, dtype, j);
-                    ss += v * v;
-                }
-            }
+            for (int e = 0; e < 8; ++e)
+                if (j0 + e < d) ss += v[e] * v[e];
         }
     }
     ss = wave_sum_f64(ss);
-    const double n = __builtin_sqrt(ss);
-    for (int j0 = lane * 8; j0 < d_pad; j0 += 512) {
-        uint16_t h[8];
+    return __builtin_sqrt(ss);
+}
+
+// Columns j0 .. j0+7 of the normalised row as packed bfloat16 (zeros beyond d, for a zero norm or dead rows).
+__device__ inline u32x4 quantise8(const void* row, int dtype, int d, int j0, double n, bool live) {
+    uint16_t h[8];
+    double v[8];
+    if (live && j0 < d && n != 0.0) load8(row, dtype, d, j0, v);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            const int j = j0 + e;
-            h[e] = 0;
-            if (live && j < d && n != 0.0) h[e] = bf16_rne_from_f64(load_in(row, dtype, j) / n);
-        }
-        u32x4 w;
-        w.x = (uint32_t)h[0] | ((uint32_t)h[1] << 16);
-        w.y = (uint32_t)h[2] | ((uint32_t)h[3] << 16);
-        w.z = (uint32_t)h[4] | ((uint32_t)h[5] << 16);
-        w.w = (uint32_t)h[6] | ((uint32_t)h[7] << 16);
-        emit(j0, w);
+    for (int e = 0; e < 8; ++e) {
+        const int j = j0 + e;
+        h[e] = 0;
+        if (live && j < d && n != 0.0) h[e] = bf16_rne_from_f64(v[e] / n);
     }
+    u32x4 w;
+    w.x = (uint32_t)h[0] | ((uint32_t)h[1] << 16);
+    w.y = (uint32_t)h[2] | ((uint32_t)h[3] << 16);
+    w.z = (uint32_t)h[4] | ((uint32_t)h[5] << 16);
+    w.w = (uint32_t)h[6] | ((uint32_t)h[7] << 16);
+    return w;
+}
+
+template <class Emit>
+__device__ inline void normalise_row(const void* row, int dtype, int d, int d_pad, bool live, int lane, Emit emit) {
+    const double n = row_norm(row, dtype, d, live, lane);
+    for (int j0 = lane * 8; j0 < d_pad; j0 += 512) emit(j0, quantise8(row, dtype, d, j0, n, live));
+}
+
+// Dot product of two packed bfloat16 chunks, accumulated into acc in float32 in column order.  bf16 x bf16
+// products are exact in float.
+__device__ inline float dot8_bf16(u32x4 a, u32x4 b, float acc) {
+    const uint32_t av[4] = {a.x, a.y, a.z, a.w}, bv[4] = {b.x, b.y, b.z, b.w};
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+        acc += __uint_as_float(av[t] << 16) * __uint_as_float(bv[t] << 16);
+        acc += __uint_as_float(av[t] & 0xFFFF0000u) * __uint_as_float(bv[t] & 0xFFFF0000u);
+    }
+    return acc;
 }
 
 // ---------------------------------------------------------------------------

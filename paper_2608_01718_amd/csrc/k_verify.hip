@@ -89,16 +89,9 @@ __global__ __launch_bounds__(256) void k_finalize_verify(
         const char* src = (const char*)M.la[mi] + (int64_t)b * M.d[mi] * esz;
         const u32x4* er = (const u32x4*)(M.emb[mi] + (int64_t)i * M.d_pad[mi]);
         float acc = 0.0f;
-        normalise_row(src, dtype, M.d[mi], M.d_pad[mi], true, lane, [&](int j0, u32x4 w) {
-            const u32x4 e = er[j0 >> 3];
-            const uint32_t av[4] = {w.x, w.y, w.z, w.w}, ev[4] = {e.x, e.y, e.z, e.w};
-#pragma unroll
-            for (int t = 0; t < 4; ++t) {
-                // bf16 x bf16 products are exact in float; padded columns are zero on both sides
-                acc += __uint_as_float(av[t] << 16) * __uint_as_float(ev[t] << 16);
-                acc += __uint_as_float(av[t] & 0xFFFF0000u) * __uint_as_float(ev[t] & 0xFFFF0000u);
-            }
-        });
+        // padded columns are zero on both sides
+        normalise_row(src, dtype, M.d[mi], M.d_pad[mi], true, lane,
+                      [&](int j0, u32x4 w) { acc = dot8_bf16(w, er[j0 >> 3], acc); });
         acc = wave_sum_f32(acc);
         const float r = fminf(fmaxf(acc, -1.0f), 1.0f);
         if (lane == 0) resp_out[(int64_t)b * M.m + mi] = r;

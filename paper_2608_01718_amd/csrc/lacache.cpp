@@ -29,6 +29,7 @@ struct lacache_s {
     int32_t* tokens = nullptr; // [cap][k_cap]
     uint16_t* qt = nullptr;    // tiled [mb_pad][d_pad] normalised queries
     uint64_t* part = nullptr;  // [max_batch][kMaxPartials] packed top-1 candidates
+    uint32_t* calib = nullptr; // [kCalibScratchWords] state and histograms of the calibration select
     bool profiling = false;
     std::vector<std::pair<hipEvent_t, hipEvent_t>> prof;
 };
@@ -59,6 +60,7 @@ void free_all(lacache_s* h) {
     (void)hipFree(h->tokens);
     (void)hipFree(h->qt);
     (void)hipFree(h->part);
+    (void)hipFree(h->calib);
     for (auto& p : h->prof) {
         (void)hipEventDestroy(p.first);
         (void)hipEventDestroy(p.second);
@@ -148,6 +150,7 @@ int lacache_create_ensemble(lacache_t* out, int64_t capacity, int32_t d, int32_t
     if (rc == LACACHE_OK) rc = alloc_zero((void**)&h->tokens, (size_t)h->cap * h->k_cap * 4);
     if (rc == LACACHE_OK) rc = alloc_zero((void**)&h->qt, (size_t)h->mb_pad * h->d_pad * 2);
     if (rc == LACACHE_OK) rc = alloc_zero((void**)&h->part, (size_t)h->max_batch * kMaxPartials * 8);
+    if (rc == LACACHE_OK) rc = alloc_zero((void**)&h->calib, (size_t)kCalibScratchWords * 4);
     if (rc == LACACHE_OK && hipDeviceSynchronize() != hipSuccess) rc = LACACHE_EHIP;
     if (rc != LACACHE_OK) {
         free_all(h);
@@ -310,6 +313,20 @@ int lacache_export_prefix(lacache_t h, int32_t model, int64_t first, int32_t n, 
 }
 
 int32_t lacache_models(lacache_t h) { return h ? h->m : -1; }
+
+int lacache_calibrate(lacache_t h, int32_t which, const void* a, const void* b, int64_t n, float percentile, float cap,
+                      float* sims, float* tau, void* stream) {
+    if (!h || which < -1 || which >= h->m || n < 1 || !std::isfinite(percentile) || percentile < 0.0f ||
+        percentile > 100.0f || !std::isfinite(cap) || !a || !b || !sims || !tau)
+        return LACACHE_EINVAL;
+    DeviceGuard g(h->device);
+    if (!g.ok) return LACACHE_EHIP;
+    const int dim = which < 0 ? h->d : h->d_resp[which];
+    if (launch_calibrate(a, b, h->dtype, dim, n, percentile, cap, sims, tau, h->calib, h->num_cu,
+                         (hipStream_t)stream) != hipSuccess)
+        return LACACHE_EHIP;
+    return LACACHE_OK;
+}
 
 int lacache_set_small_batch(lacache_t h, int32_t b_small) {
     if (!h || b_small < 0 || b_small > 16 * stream_max_qg(h->d_pad)) return LACACHE_EINVAL;

@@ -49,6 +49,13 @@ hipError_t launch_finalize_verify(const uint64_t* part, int P, bool part_groups,
                                   int k_cap, float tau_q, int32_t* idx, float* score, float* resp_score,
                                   int32_t* decision, hipStream_t s);
 
+// Threshold calibration over n pairs (a[j], b[j]) of d-dimensional input vectors: sims[j] = the lookup's
+// cosine of the pair; tau[0] = the percentile (linear between the closest ranks), tau[1] = min(cap, tau[0]).
+// scratch: kCalibScratchWords words of device memory.
+constexpr int kCalibScratchWords = 64 + 2 * 2048;
+hipError_t launch_calibrate(const void* a, const void* b, int dtype, int d, int64_t n, float percentile, float cap,
+                            float* sims, float* tau, uint32_t* scratch, int num_cu, hipStream_t s);
+
 // Most partials a stage-1 launch may write per query.
 constexpr int kMaxPartials = 1024;
 

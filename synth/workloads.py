@@ -367,6 +367,35 @@ def ensemble_lookahead(sp: Spec, d_models, stored, tokens, q: dict, stream_chunk
     return out, la_tok
 
 
+_S_CAL_X, _S_CAL_V, _S_CAL_C = 60, 61, 62
+
+
+def calibration_pairs(n: int, d: int, cos_lo: float, cos_hi: float, seed: int, in_dtype: int = BF16,
+                      threads: int | None = None):
+    """n benign pairs for threshold calibration: x_j = unit(N(0, I)) and y_j = c_j x_j + sqrt(1 - c_j^2) v_j
+    with v_j a random unit vector orthogonal to x_j and c_j ~ U[cos_lo, cos_hi], so cos(x_j, y_j) = c_j before
+    rounding (the paraphrase-pair query cosines of Appendix A.2 lie in such a band: P5 = 0.857 for BGE).
+    Returns (a, b), [n][d] in the given input dtype."""
+    dt = np.float32 if in_dtype == F32 else np.uint16
+    a = np.empty((n, d), dt)
+    b = np.empty((n, d), dt)
+
+    def work(c):
+        r0 = c * GEN_CHUNK
+        r1 = min(n, r0 + GEN_CHUNK)
+        m = r1 - r0
+        x = _unit_rows(_rng(seed, _S_CAL_X, c).standard_normal((m, d), dtype=np.float32))
+        v = _orth_unit(_rng(seed, _S_CAL_V, c), x)
+        cs = _rng(seed, _S_CAL_C, c).uniform(cos_lo, cos_hi, (m, 1))
+        a[r0:r1] = _cast(x, in_dtype)
+        b[r0:r1] = _cast(cs * x + np.sqrt(1 - cs * cs) * v, in_dtype)
+
+    chunks = range((n + GEN_CHUNK - 1) // GEN_CHUNK)
+    with ThreadPoolExecutor(threads or min(16, os.cpu_count() or 1)) as ex:
+        list(ex.map(work, chunks))
+    return a, b
+
+
 def generate(sp: Spec | str, threads: int | None = None, **overrides) -> Workload:
     """Build the cache contents and one batch of queries for a spec."""
     if isinstance(sp, str):
@@ -385,4 +414,4 @@ def generate(sp: Spec | str, threads: int | None = None, **overrides) -> Workloa
 __all__ = ["Spec", "Workload", "CONFIGS", "spec", "generate", "entries", "queries", "to_bf16_bits",
            "bf16_bits_to_f64", "as_f64", "CLS_MISS", "CLS_BENIGN", "CLS_COLLISION",
            "F32", "BF16", "GEN_CHUNK", "SERVE_SMALL_CALL_B", "ENSEMBLE_DIMS", "ensemble_entries",
-           "ensemble_lookahead"]
+           "ensemble_lookahead", "calibration_pairs"]

@@ -88,6 +88,9 @@ def test_argument_checks_before_any_device_work(lib):
     assert lib.lacache_lookup_ensemble(None, None, None, None, 0, 0.5, None, 1, None, None, None, None, None) == EINVAL
     lib.lacache_export_prefix.argtypes = [P, ctypes.c_int32, ctypes.c_int64, ctypes.c_int32, P, P]
     assert lib.lacache_export_prefix(None, 0, 0, 0, None, None) == EINVAL
+    lib.lacache_calibrate.argtypes = [P, ctypes.c_int32, P, P, ctypes.c_int64, ctypes.c_float, ctypes.c_float, P, P,
+                                      P]
+    assert lib.lacache_calibrate(None, -1, None, None, 1, 5.0, 0.8, None, None, None) == EINVAL
     lib.lacache_strerror.restype = ctypes.c_char_p
     assert lib.lacache_strerror(-2) == b"cache capacity exceeded"
     assert lib.lacache_strerror(12345) == b"unknown error code"
