@@ -13,7 +13,8 @@ Section 5.1); for hits only, the lookahead check on the matched entry --
 identical first-k tokens, or prefix-embedding cosine >= tau_r (Algorithm 1,
 Section 4.2 cache structure, Section 5.1); with m lookahead models, all m
 checks (Section 4.4); thresholds from benign pairs as capped percentiles of
-their cosines (Appendix A.2).
+their cosines (Appendix A.2); the speculative-decoding acceptance length of
+the draft tokens (Section 4.3).
 """
 from __future__ import annotations
 
@@ -63,6 +64,7 @@ def lib():
         f64 = ctypes.c_double
         L.lco_threshold_rule.argtypes = [P, i64, f64, f64, P, P]
         L.lco_calibrate.argtypes = [P, P, i64, i32, f64, f64, P, P, P]
+        L.lco_accept_length.argtypes = [P, i32, i32, P, P, i32, i32, P, P]
         L.lco_first_identical.restype = i64
         L.lco_num_threads.restype = ctypes.c_int
         L.lco_lookup_ensemble.argtypes = [P, i64, i32, P, i32, f32, i32, P, P, P, P, P, i32, P, i32, P, P, P, P]
@@ -204,6 +206,20 @@ def calibrate(a_q, b_q, p: float, cap: float) -> dict:
     lib().lco_calibrate(_ptr(a_q), _ptr(b_q), n, d, float(p), float(cap), _ptr(sims), ctypes.byref(P),
                         ctypes.byref(tau))
     return dict(sims=sims, P=P.value, tau=tau.value)
+
+
+def accept_length(logits, dtype: int, tokens, p_draft) -> dict:
+    """Speculative-decoding acceptance (Section 4.3).  logits: [B][k][V] float32, or bfloat16 bits (uint16)
+    with dtype BF16; tokens: [B][k] int32; p_draft: [B][k] float32.  Returns accept_len [B] and p_target
+    [B][k] (float64)."""
+    logits = np.ascontiguousarray(logits, np.float32 if dtype == F32 else np.uint16)
+    B, k, V = logits.shape
+    tokens = _c(tokens, np.int32).reshape(B, k)
+    p_draft = np.ascontiguousarray(p_draft, np.float32).reshape(B, k)
+    out = dict(accept_len=np.empty(B, np.int32), p_target=np.empty((B, k), np.float64))
+    lib().lco_accept_length(_ptr(logits), dtype, V, _ptr(tokens), _ptr(p_draft), B, k, _ptr(out["accept_len"]),
+                            _ptr(out["p_target"]))
+    return out
 
 
 def num_threads() -> int:

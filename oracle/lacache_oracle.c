@@ -29,6 +29,8 @@
  *
  *   calibrate Thresholds from benign pairs (Appendix A.2): the p-th percentile
  *             of the pair cosines, capped from above.
+ *   accept    Speculative-decoding acceptance after a miss or rejection
+ *             (Section 4.3): leading draft tokens with P_f(t) >= P_g(t).
  *
  * Decision codes: 0 MISS, 1 REJECT (collision detected), 2 HIT, 3 HIT_EXACT.
  */
@@ -386,4 +388,44 @@ void lco_calibrate(const uint16_t *a, const uint16_t *b, int64_t n, int32_t d, d
         sims[j] = s > 1.0 ? 1.0 : (s < -1.0 ? -1.0 : s);
     }
     lco_threshold_rule(sims, n, p, cap, P_out, tau_out);
+}
+
+/*
+ * Speculative-decoding acceptance (Section 4.3, speculative decoding): after a
+ * miss or a rejected lookahead, the k draft tokens t_1..t_k of the draft model
+ * g are verified by the target model f in one forward pass; token t_j is
+ * accepted when P_f(t_j) >= P_g(t_j), starting from the first token, and f
+ * takes over at the first token that fails.  P_f(t) is the softmax probability
+ * of t under f's logits at that position.  The accepted length is the number
+ * of leading accepted tokens (0 .. k).
+ *
+ *   logits      [B][k][V] (dtype 0 float32, 1 bfloat16): f's logits at each draft position
+ *   tokens      [B][k] draft token IDs; an ID outside [0, V) has probability 0
+ *   p_draft     [B][k] P_g of each draft token (float32)
+ * Outputs: accept_len [B]; p_target [B][k] = P_f(t_j) in double (max-shifted
+ * exponentials summed in index order).
+ */
+void lco_accept_length(const void *logits, int32_t dtype, int32_t V, const int32_t *tokens, const float *p_draft,
+                       int32_t B, int32_t k, int32_t *accept_len, double *p_target)
+{
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t row = 0; row < (int64_t)B * k; ++row) {
+        double m = -INFINITY;
+        for (int32_t v = 0; v < V; ++v) {
+            double x = read_in(logits, dtype, row, V, v);
+            if (x > m)
+                m = x;
+        }
+        double s = 0.0;
+        for (int32_t v = 0; v < V; ++v)
+            s += exp(read_in(logits, dtype, row, V, v) - m);
+        int32_t t = tokens[row];
+        p_target[row] = (t >= 0 && t < V) ? exp(read_in(logits, dtype, row, V, t) - m) / s : 0.0;
+    }
+    for (int32_t b = 0; b < B; ++b) {
+        int32_t len = 0;
+        while (len < k && p_target[(int64_t)b * k + len] >= (double)p_draft[(int64_t)b * k + len])
+            ++len;
+        accept_len[b] = len;
+    }
 }

@@ -40,6 +40,17 @@ MUTANTS = {
         "P = x[lo] + (h - (double)lo) * (x[lo + 1] - x[lo]);", "P = x[lo + 1];"),
     "cap applied as a floor": ("*tau_out = fmin(cap, P);", "*tau_out = fmax(cap, P);"),
     "similarities sorted descending": ("return (a > b) - (a < b);", "return (a < b) - (a > b);"),
+    "draft accepted only when P_f > P_g": (
+        "p_target[(int64_t)b * k + len] >= (double)p_draft", "p_target[(int64_t)b * k + len] > (double)p_draft"),
+    "acceptance counts every accepted token, not the leading run": (
+        "        while (len < k && p_target[(int64_t)b * k + len] >= (double)p_draft[(int64_t)b * k + len])\n"
+        "            ++len;",
+        "        for (int32_t j = 0; j < k; ++j)\n"
+        "            len += p_target[(int64_t)b * k + j] >= (double)p_draft[(int64_t)b * k + j];"),
+    "softmax without the max shift": ("s += exp(read_in(logits, dtype, row, V, v) - m);",
+                                      "s += exp(read_in(logits, dtype, row, V, v));"),
+    "probability read at the next vocabulary entry": ("exp(read_in(logits, dtype, row, V, t) - m) / s",
+                                                      "exp(read_in(logits, dtype, row, V, (t + 1) % V) - m) / s"),
 }
 
 

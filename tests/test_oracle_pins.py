@@ -559,3 +559,77 @@ def test_calibration_reproduces_the_paper_table():
             P, tau = oracle.threshold_rule(x, p, row["cap"])
             assert P == row[key], (name, P)
             assert abs(tau - row["used"]) <= 1e-12, (name, tau, row["used"])
+
+
+# --------------------------------------------------------------------------- speculative-decoding acceptance (Section 4.3)
+
+
+def _softmax_rows(x):
+    import scipy.special
+    return scipy.special.softmax(np.asarray(x, np.float64), axis=-1)
+
+
+@pytest.mark.parametrize("dtype", [oracle.F32, oracle.BF16])
+def test_accept_length_matches_bruteforce(dtype):
+    rng = np.random.default_rng(71 + dtype)
+    B, k, V = 6, 9, 1000
+    lg = (rng.standard_normal((B, k, V)) * 3.0).astype(np.float32)
+    if dtype == oracle.BF16:
+        lg_in = synth.to_bf16_bits(lg)
+        lg = synth.bf16_bits_to_f64(lg_in).astype(np.float64)
+    else:
+        lg_in = lg
+    tok = rng.integers(0, V, (B, k), dtype=np.int32)
+    tok[:, ::2] = np.argmax(lg, axis=-1)[:, ::2]           # some likely tokens
+    P = _softmax_rows(lg)
+    pt = np.take_along_axis(P, tok[..., None], axis=-1)[..., 0]
+    pd = (pt * np.exp(rng.normal(0, 0.7, (B, k)))).astype(np.float32)
+    o = oracle.accept_length(lg_in, dtype, tok, pd)
+    np.testing.assert_allclose(o["p_target"], pt, rtol=1e-12, atol=0)
+    acc = pt >= pd.astype(np.float64)
+    want = np.array([np.argmin(np.append(a, False)) for a in acc])      # first rejection (k if none)
+    np.testing.assert_array_equal(o["accept_len"], want)
+    assert 0 < want.sum() < B * k
+
+
+def test_accept_length_closed_forms():
+    V, k = 4, 6
+    zeros = np.zeros((1, k, V), np.float32)              # uniform: P_f = 1/4 exactly
+    tok = np.zeros((1, k), np.int32)
+    assert np.all(oracle.accept_length(zeros, oracle.F32, tok, np.full((1, k), 0.25, np.float32))["p_target"] == 0.25)
+    # equality accepts (the rule is P_f >= P_g)
+    assert oracle.accept_length(zeros, oracle.F32, tok, np.full((1, k), 0.25, np.float32))["accept_len"][0] == k
+    assert oracle.accept_length(zeros, oracle.F32, tok, np.full((1, k), np.nextafter(np.float32(0.25), 1), np.float32))[
+        "accept_len"][0] == 0
+    assert oracle.accept_length(zeros, oracle.F32, tok, np.zeros((1, k), np.float32))["accept_len"][0] == k
+    assert oracle.accept_length(zeros, oracle.F32, tok, np.full((1, k), 1.5, np.float32))["accept_len"][0] == 0
+    # only the leading run counts: accept, accept, reject, accept, ... -> 2
+    pd = np.array([[0.1, 0.2, 0.3, 0.1, 0.1, 0.1]], np.float32)
+    assert oracle.accept_length(zeros, oracle.F32, tok, pd)["accept_len"][0] == 2
+    # one dominant logit: P_f ~ 1 without overflow; an out-of-range token has probability 0
+    big = np.zeros((1, 2, 50), np.float32)
+    big[0, :, 7] = 1000.0
+    o = oracle.accept_length(big, oracle.F32, np.array([[7, 50]], np.int32), np.array([[0.99, 0.0]], np.float32))
+    assert abs(o["p_target"][0, 0] - 1.0) < 1e-12 and o["p_target"][0, 1] == 0.0 and o["accept_len"][0] == 2
+
+
+def test_accept_length_invariances():
+    rng = np.random.default_rng(73)
+    B, k, V = 4, 8, 300
+    # logits on a 2^-10 grid, so that adding 8 is exact in float32
+    lg = (np.round(rng.standard_normal((B, k, V)) * 2 * 1024) / 1024).astype(np.float32)
+    tok = rng.integers(0, V, (B, k), dtype=np.int32)
+    pd = rng.uniform(0, 0.02, (B, k)).astype(np.float32)
+    base = oracle.accept_length(lg, oracle.F32, tok, pd)
+    assert np.array_equal((lg + np.float32(8.0)).astype(np.float64), lg.astype(np.float64) + 8.0)
+    shifted = oracle.accept_length(lg + np.float32(8.0), oracle.F32, tok, pd)
+    np.testing.assert_allclose(shifted["p_target"], base["p_target"], rtol=1e-12)
+    perm = rng.permutation(V)
+    inv = np.argsort(perm)
+    permuted = oracle.accept_length(lg[..., perm], oracle.F32, inv[tok].astype(np.int32), pd)
+    np.testing.assert_allclose(permuted["p_target"], base["p_target"], rtol=1e-12)
+    prev = base["accept_len"]
+    for f in (1.5, 3.0, 10.0):                                        # stricter drafts never accept more
+        cur = oracle.accept_length(lg, oracle.F32, tok, (pd * f).astype(np.float32))["accept_len"]
+        assert np.all(cur <= prev)
+        prev = cur
