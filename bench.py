@@ -11,8 +11,9 @@ The headline workload (`value`) is serve_large: 4096 queries per call (the
 matrix-core-bound regime); serve_small (16 queries per call, the HBM-bound
 regime) is measured in the same run and reported under "secondary", and the
 same keys with the four-model lookahead ensemble (Section 4.4) under
-"ensemble", and threshold calibration over a million benign pairs
-(Appendix A.2) under "calibration".  For
+"ensemble", threshold calibration over a million benign pairs
+(Appendix A.2) under "calibration", and the speculative-decoding acceptance
+of 256 x 20 draft tokens (Section 4.3) under "accept".  For
 each, "roofline" rates the stage-1 kernel, timed with HIP events recorded by
 the library on the launch stream, against the MI355X peak (bf16 dense MFMA
 2.5 PFLOP/s, HBM 8 TB/s).  "cpu_baseline" times the CPU oracle on a bounded
@@ -48,6 +49,7 @@ def parse():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
     ap.add_argument("--no-ensemble", action="store_true", help="skip the lookahead-ensemble measurement")
     ap.add_argument("--no-calibration", action="store_true", help="skip the threshold-calibration measurement")
+    ap.add_argument("--no-accept", action="store_true", help="skip the speculative-decoding acceptance measurement")
     ap.add_argument("--no-probe", action="store_true",
                     help="skip the attainable-ceiling probe (sustained MFMA rate on random bf16, HBM streaming read)")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
@@ -305,6 +307,38 @@ def run_calibration(steps, warmup, lc, torch, synth):
                 pair_read_gbs=pair_bytes / (ms * 1e-3) / 1e9)
 
 
+def run_accept(steps, warmup, lc, torch, synth):
+    """Speculative-decoding acceptance (Section 4.3) for 256 missed or rejected queries with k = 20 draft
+    tokens over a 128,256-token vocabulary: the target's bf16 logits at the 20 positions (1.31 GB) are read
+    once; one step is one lacache_accept_length call."""
+    from tests.gpu_util import to_dev
+    B, k, V = 256, 20, 128256
+    t0 = time.time()
+    lg, tok, pd = synth.draft_verification(B, k, V, seed=12)
+    log(f"[bench] acceptance: generated in {time.time() - t0:.1f}s")
+    lgd, tokd, pdd = to_dev(lg), to_dev(tok), to_dev(pd)
+    del lg
+    dev = torch.device("cuda", 0)
+    out = (torch.empty(B, dtype=torch.int32, device=dev), torch.empty((B, k), dtype=torch.float32, device=dev))
+    for _ in range(warmup):
+        lc.lacache_accept_length(lgd, tokd, pdd, out=out)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        lc.lacache_accept_length(lgd, tokd, pdd, out=out)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    mean_len = float(out[0].float().mean().item())
+    del lgd, tokd, pdd, out
+    torch.cuda.empty_cache()
+    logit_bytes = 2.0 * B * k * V
+    return dict(workload=f"{B} queries x k = {k} draft tokens, vocabulary {V:,}, bf16 target logits",
+                value=B / (ms * 1e-3), unit="queries/s", ms_per_step=ms, mean_accepted=mean_len,
+                logits_read_gbs=logit_bytes / (ms * 1e-3) / 1e9)
+
+
 def cpu_baseline(sp, w, call_b):
     """The CPU oracle, as it is, on a bounded sample: a few queries against the full cache."""
     import oracle
@@ -354,6 +388,7 @@ def main():
 
     ensemble = None if args.no_ensemble else run_ensemble(args.steps, args.warmup, lc, torch, synth)
     calibration = None if args.no_calibration else run_calibration(args.steps, args.warmup, lc, torch, synth)
+    accept = None if args.no_accept else run_accept(args.steps, args.warmup, lc, torch, synth)
 
     line = {
         "metric": "cache lookups/sec (2-stage) at N=1M,d=768; % HBM / MFMA roofline",
@@ -385,6 +420,8 @@ def main():
         line["ensemble"] = ensemble
     if calibration:
         line["calibration"] = calibration
+    if accept:
+        line["accept"] = accept
     if probe:
         # the same kernels rated against what this GPU sustains: MFMA throughput on random bf16 operands
         # (operand-dependent power lowers the clock below the datasheet's) and a plain streaming read

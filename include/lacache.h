@@ -205,6 +205,26 @@ int lacache_calibrate(lacache_t h, int32_t which, const void *a, const void *b, 
                       float cap, float *sims, float *tau, void *stream);
 
 /*
+ * Speculative-decoding acceptance after a miss or a rejected lookahead
+ * (Section 4.3): the k draft tokens of the draft model g are verified by the
+ * target model f in one forward pass; token t_j is accepted when
+ * P_f(t_j) >= P_g(t_j), from the first token on, and f takes over at the
+ * first failure.  Needs no cache handle; runs on the calling thread's current
+ * device.
+ *   logits        [B][k][V] (dtype): f's logits at each draft position
+ *   draft_tokens  [B][k] int32 draft token IDs; an ID outside [0, V) has probability 0
+ *   p_draft       [B][k] float: P_g of each draft token
+ *   1 <= V, 0 <= B, 1 <= k <= 4096
+ * Outputs: p_target [B][k] float = softmax(logits[b][j])[t_j] (float32
+ * arithmetic, max-shifted exponentials); accept_len [B] int32 = the number
+ * of leading positions with p_target >= p_draft (0 .. k).  Every row needs at
+ * least one finite logit.  B == 0 is a no-op.
+ */
+int lacache_accept_length(const void *logits, lacache_dtype dtype, int32_t V, const int32_t *draft_tokens,
+                          const float *p_draft, int32_t B, int32_t k, int32_t *accept_len, float *p_target,
+                          void *stream);
+
+/*
  * Batch-size crossover of stage 1: batches of at most b_small queries use the
  * bandwidth-bound streaming kernel, larger ones the matrix-core GEMM kernel.
  * 0 <= b_small <= 64 (default 64; 0 sends every batch to the GEMM kernel).

@@ -37,6 +37,7 @@ _lib.lacache_lookup_ensemble.argtypes = [_P, _P, ctypes.POINTER(_P), _P, _i32, _
                                          _P, _P, _P, _P, _P]
 _lib.lacache_export_prefix.argtypes = [_P, _i32, _i64, _i32, _P, _P]
 _lib.lacache_calibrate.argtypes = [_P, _i32, _P, _P, _i64, _f32, _f32, _P, _P, _P]
+_lib.lacache_accept_length.argtypes = [_P, ctypes.c_int, _i32, _P, _P, _i32, _i32, _P, _P, _P]
 _lib.lacache_destroy.argtypes = [_P]
 _lib.lacache_insert.argtypes = [_P, _P, _P, _P, _i32, ctypes.POINTER(_i64), _P]
 _lib.lacache_lookup.argtypes = [_P, _P, _P, _P, _i32, _f32, _f32, _i32, _P, _P, _P, _P, _P]
@@ -51,7 +52,8 @@ _lib.lacache_strerror.restype = ctypes.c_char_p
 
 EXPORTED = ("lacache_create", "lacache_create_ensemble", "lacache_models", "lacache_destroy", "lacache_insert",
             "lacache_insert_ensemble", "lacache_lookup", "lacache_lookup_ensemble", "lacache_size",
-            "lacache_export", "lacache_export_prefix", "lacache_calibrate", "lacache_set_small_batch",
+            "lacache_export", "lacache_export_prefix", "lacache_calibrate", "lacache_accept_length",
+            "lacache_set_small_batch",
             "lacache_profile", "lacache_profile_read", "lacache_strerror")
 
 
@@ -303,6 +305,31 @@ def lacache_calibrate(c: LaCache, which: int, a, b, percentile: float, cap: floa
     _check(_lib.lacache_calibrate(c.handle, int(which), _vec(a, c.in_dtype, n, dim, c.device, "a"),
                                   _vec(b, c.in_dtype, n, dim, c.device, "b"), n, float(percentile), float(cap),
                                   sims.data_ptr(), tau.data_ptr(), _stream(c.device, stream)), "lacache_calibrate")
+    return out
+
+
+def lacache_accept_length(logits, draft_tokens, p_draft, out=None, stream=None):
+    """Speculative-decoding acceptance (Section 4.3).  logits: [B][k][V] float32 or bfloat16 (int16/uint16
+    bits) on a GPU; draft_tokens [B][k] int32; p_draft [B][k] float32.  Returns (accept_len int32 [B],
+    p_target float32 [B][k]) on the same device."""
+    if logits.dim() != 3 or logits.device.type != "cuda" or not logits.is_contiguous():
+        raise ValueError("logits: expected a contiguous [B, k, V] tensor on a GPU")
+    B, k, V = logits.shape
+    dtype = F32 if logits.dtype == torch.float32 else BF16
+    if dtype == BF16 and logits.dtype not in (torch.bfloat16, torch.int16, torch.uint16):
+        raise ValueError(f"logits: unsupported dtype {logits.dtype}")
+    dev = logits.device
+    for t, dt, nm in ((draft_tokens, torch.int32, "draft_tokens"), (p_draft, torch.float32, "p_draft")):
+        if t.dtype != dt or t.device != dev or tuple(t.shape) != (B, k) or not t.is_contiguous():
+            raise ValueError(f"{nm}: expected a contiguous [{B}, {k}] {dt} tensor on {dev}")
+    if out is None:
+        out = (torch.empty(B, dtype=torch.int32, device=dev), torch.empty((B, k), dtype=torch.float32, device=dev))
+    acc, pt = out
+    if acc.dtype != torch.int32 or acc.numel() != B or pt.dtype != torch.float32 or pt.numel() != B * k:
+        raise ValueError("out: expected (int32 [B], float32 [B, k])")
+    _check(_lib.lacache_accept_length(logits.data_ptr(), dtype, V, draft_tokens.data_ptr(), p_draft.data_ptr(), B, k,
+                                      acc.data_ptr(), pt.data_ptr(), _stream(dev.index, stream)),
+           "lacache_accept_length")
     return out
 
 

@@ -328,6 +328,18 @@ int lacache_calibrate(lacache_t h, int32_t which, const void* a, const void* b, 
     return LACACHE_OK;
 }
 
+int lacache_accept_length(const void* logits, lacache_dtype dtype, int32_t V, const int32_t* draft_tokens,
+                          const float* p_draft, int32_t B, int32_t k, int32_t* accept_len, float* p_target,
+                          void* stream) {
+    if (V < 1 || B < 0 || k < 1 || k > 4096 || (dtype != LACACHE_F32 && dtype != LACACHE_BF16)) return LACACHE_EINVAL;
+    if (B == 0) return LACACHE_OK;
+    if (!logits || !draft_tokens || !p_draft || !accept_len || !p_target) return LACACHE_EINVAL;
+    if (launch_accept_length(logits, (int)dtype, V, draft_tokens, p_draft, B, k, accept_len, p_target,
+                             (hipStream_t)stream) != hipSuccess)
+        return LACACHE_EHIP;
+    return LACACHE_OK;
+}
+
 int lacache_set_small_batch(lacache_t h, int32_t b_small) {
     if (!h || b_small < 0 || b_small > 16 * stream_max_qg(h->d_pad)) return LACACHE_EINVAL;
     h->b_small = b_small;

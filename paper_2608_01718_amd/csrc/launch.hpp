@@ -56,6 +56,11 @@ constexpr int kCalibScratchWords = 64 + 2 * 2048;
 hipError_t launch_calibrate(const void* a, const void* b, int dtype, int d, int64_t n, float percentile, float cap,
                             float* sims, float* tau, uint32_t* scratch, int num_cu, hipStream_t s);
 
+// Speculative-decoding acceptance: p_target[b][j] = softmax(logits[b][j])[tokens[b][j]] (0 for an
+// out-of-range token); accept_len[b] = the number of leading positions with p_target >= p_draft.
+hipError_t launch_accept_length(const void* logits, int dtype, int V, const int32_t* tokens, const float* p_draft,
+                                int B, int k, int32_t* accept_len, float* p_target, hipStream_t s);
+
 // Most partials a stage-1 launch may write per query.
 constexpr int kMaxPartials = 1024;
 

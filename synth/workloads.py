@@ -396,6 +396,40 @@ def calibration_pairs(n: int, d: int, cos_lo: float, cos_hi: float, seed: int, i
     return a, b
 
 
+_S_SD_LOG, _S_SD_TOP, _S_SD_TOK, _S_SD_PD = 70, 71, 72, 73
+
+
+def draft_verification(B: int, k: int, V: int, seed: int, in_dtype: int = BF16, frac_top: float = 0.9,
+                       threads: int | None = None):
+    """Inputs of the speculative-decoding acceptance step (Section 4.3) for B queries with k draft tokens.
+
+    The target model's logits at each draft position are N(0, 1) over the vocabulary with one favoured
+    token raised by U[12, 16] (a peaked next-token distribution).  A fraction frac_top of the draft tokens
+    is the favoured token, drawn with a draft probability U[0.1, 0.6]; the rest are uniform random tokens
+    with draft probability U[0, 2e-6].  Returns (logits [B][k][V] in the input dtype, tokens [B][k] int32,
+    p_draft [B][k] float32)."""
+    rows = B * k
+    logits = np.empty((rows, V), np.float32 if in_dtype == F32 else np.uint16)
+    top = _rng(seed, _S_SD_TOP).integers(0, V, rows)
+    boost = _rng(seed, _S_SD_TOP, 1).uniform(12.0, 16.0, rows)
+    chunk = max(1, (1 << 22) // V)
+
+    def work(c):
+        r0, r1 = c * chunk, min(rows, (c + 1) * chunk)
+        x = _rng(seed, _S_SD_LOG, c).standard_normal((r1 - r0, V), dtype=np.float32)
+        x[np.arange(r1 - r0), top[r0:r1]] += boost[r0:r1].astype(np.float32)
+        logits[r0:r1] = x if in_dtype == F32 else to_bf16_bits(x)
+
+    with ThreadPoolExecutor(threads or min(16, os.cpu_count() or 1)) as ex:
+        list(ex.map(work, range((rows + chunk - 1) // chunk)))
+    g = _rng(seed, _S_SD_TOK)
+    fav = g.random(rows) < frac_top
+    tokens = np.where(fav, top, g.integers(0, V, rows)).astype(np.int32)
+    pr = _rng(seed, _S_SD_PD)
+    p_draft = np.where(fav, pr.uniform(0.1, 0.6, rows), pr.uniform(0.0, 2e-6, rows)).astype(np.float32)
+    return logits.reshape(B, k, V), tokens.reshape(B, k), p_draft.reshape(B, k)
+
+
 def generate(sp: Spec | str, threads: int | None = None, **overrides) -> Workload:
     """Build the cache contents and one batch of queries for a spec."""
     if isinstance(sp, str):
@@ -414,4 +448,4 @@ def generate(sp: Spec | str, threads: int | None = None, **overrides) -> Workloa
 __all__ = ["Spec", "Workload", "CONFIGS", "spec", "generate", "entries", "queries", "to_bf16_bits",
            "bf16_bits_to_f64", "as_f64", "CLS_MISS", "CLS_BENIGN", "CLS_COLLISION",
            "F32", "BF16", "GEN_CHUNK", "SERVE_SMALL_CALL_B", "ENSEMBLE_DIMS", "ensemble_entries",
-           "ensemble_lookahead", "calibration_pairs"]
+           "ensemble_lookahead", "calibration_pairs", "draft_verification"]

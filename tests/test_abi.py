@@ -91,6 +91,13 @@ def test_argument_checks_before_any_device_work(lib):
     lib.lacache_calibrate.argtypes = [P, ctypes.c_int32, P, P, ctypes.c_int64, ctypes.c_float, ctypes.c_float, P, P,
                                       P]
     assert lib.lacache_calibrate(None, -1, None, None, 1, 5.0, 0.8, None, None, None) == EINVAL
+    lib.lacache_accept_length.argtypes = [P, ctypes.c_int, ctypes.c_int32, P, P, ctypes.c_int32, ctypes.c_int32, P,
+                                          P, P]
+    assert lib.lacache_accept_length(None, 1, 0, None, None, 1, 1, None, None, None) == EINVAL     # V = 0
+    assert lib.lacache_accept_length(None, 1, 10, None, None, 1, 0, None, None, None) == EINVAL    # k = 0
+    assert lib.lacache_accept_length(None, 7, 10, None, None, 1, 1, None, None, None) == EINVAL    # dtype
+    assert lib.lacache_accept_length(None, 1, 10, None, None, 1, 1, None, None, None) == EINVAL    # null
+    assert lib.lacache_accept_length(None, 1, 10, None, None, 0, 1, None, None, None) == 0         # B = 0
     lib.lacache_strerror.restype = ctypes.c_char_p
     assert lib.lacache_strerror(-2) == b"cache capacity exceeded"
     assert lib.lacache_strerror(12345) == b"unknown error code"
