@@ -14,7 +14,8 @@ identical first-k tokens, or prefix-embedding cosine >= tau_r (Algorithm 1,
 Section 4.2 cache structure, Section 5.1); with m lookahead models, all m
 checks (Section 4.4); thresholds from benign pairs as capped percentiles of
 their cosines (Appendix A.2); the speculative-decoding acceptance length of
-the draft tokens (Section 4.3).
+the draft tokens (Section 4.3); stage 1 through a random-hyperplane LSH index
+with exact re-ranking of the candidates (Eq. (1)).
 """
 from __future__ import annotations
 
@@ -65,6 +66,9 @@ def lib():
         L.lco_threshold_rule.argtypes = [P, i64, f64, f64, P, P]
         L.lco_calibrate.argtypes = [P, P, i64, i32, f64, f64, P, P, P]
         L.lco_accept_length.argtypes = [P, i32, i32, P, P, i32, i32, P, P]
+        L.lco_simhash.argtypes = [P, i64, i32, P, i32, P, P]
+        L.lco_lookup_lsh.argtypes = [P, P, P, P, i64, i32, i32, i32, P, P, P, P, i32, i32, f32, f32, i32, P, P, P,
+                                     P, P]
         L.lco_first_identical.restype = i64
         L.lco_num_threads.restype = ctypes.c_int
         L.lco_lookup_ensemble.argtypes = [P, i64, i32, P, i32, f32, i32, P, P, P, P, P, i32, P, i32, P, P, P, P]
@@ -219,6 +223,40 @@ def accept_length(logits, dtype: int, tokens, p_draft) -> dict:
     out = dict(accept_len=np.empty(B, np.int32), p_target=np.empty((B, k), np.float64))
     lib().lco_accept_length(_ptr(logits), dtype, V, _ptr(tokens), _ptr(p_draft), B, k, _ptr(out["accept_len"]),
                             _ptr(out["p_target"]))
+    return out
+
+
+def simhash(z_q, hyperplanes, bits: int):
+    """Random-hyperplane signatures of quantised vectors z_q [n][d] under bf16 hyperplanes [bits][d].
+    Returns (sig uint32 [n][bits/32], proj float64 [n][bits])."""
+    z_q = _c(z_q, np.uint16)
+    n, d = z_q.shape
+    r = _c(hyperplanes, np.uint16).reshape(bits, d)
+    assert bits % 32 == 0
+    sig = np.empty((n, bits // 32), np.uint32)
+    proj = np.empty((n, bits), np.float64)
+    lib().lco_simhash(_ptr(z_q), n, d, _ptr(r), bits, _ptr(sig), _ptr(proj))
+    return sig, proj
+
+
+def lookup_lsh(keys_q, emb_q, tokens, sig_keys, q_q, sig_q, a_q, u, radius: int, tau_q: float, tau_r: float,
+               k: int) -> dict:
+    """Two-stage lookup with the LSH index as stage 1 (candidates within `radius` differing bits).
+    Returns idx, score, resp_score, decision, n_cand."""
+    keys_q, emb_q, tokens, N, d, k_cap = _check_store(keys_q, emb_q, tokens)
+    sig_keys = _c(sig_keys, np.uint32)
+    words = sig_keys.shape[1]
+    q_q = _c(q_q, np.uint16).reshape(-1, d)
+    B = q_q.shape[0]
+    sig_q = _c(sig_q, np.uint32).reshape(B, words)
+    a_q = _c(a_q, np.uint16).reshape(B, d)
+    u = _c(u, np.int32).reshape(B, -1)
+    out = dict(idx=np.empty(B, np.int32), score=np.empty(B, np.float32), resp_score=np.empty(B, np.float32),
+               decision=np.empty(B, np.int32), n_cand=np.empty(B, np.int32))
+    lib().lco_lookup_lsh(_ptr(keys_q), _ptr(emb_q), _ptr(tokens), _ptr(sig_keys), N, d, k_cap, words * 32,
+                         _ptr(q_q), _ptr(sig_q), _ptr(a_q), _ptr(u), B, int(radius), tau_q, tau_r, k,
+                         _ptr(out["idx"]), _ptr(out["score"]), _ptr(out["resp_score"]), _ptr(out["decision"]),
+                         _ptr(out["n_cand"]))
     return out
 
 

@@ -31,6 +31,9 @@
  *             of the pair cosines, capped from above.
  *   accept    Speculative-decoding acceptance after a miss or rejection
  *             (Section 4.3): leading draft tokens with P_f(t) >= P_g(t).
+ *   lsh       Stage 1 through a locality-sensitive index (Eq. (1)): random
+ *             hyperplane signatures, candidates within a Hamming radius,
+ *             exact re-ranking of the candidates.
  *
  * Decision codes: 0 MISS, 1 REJECT (collision detected), 2 HIT, 3 HIT_EXACT.
  */
@@ -173,6 +176,12 @@ static int32_t decide_one(const uint16_t *keys, const uint16_t *emb, const int32
     return (r >= tau_r) ? LCO_HIT : LCO_REJECT;
 }
 
+/* A scan in index order replaces its best only on a strictly larger score: the lowest index wins exact ties. */
+static int better(double s, double best)
+{
+    return s > best;
+}
+
 /*
  * Stage 1 (Algorithm 1, search with the query key): the entry of highest
  * similarity, scanning entries in index order and replacing the best only on a
@@ -186,7 +195,7 @@ static int64_t top1(const uint16_t *keys, int64_t N, int32_t d, const uint16_t *
     int64_t bi = -1;
     for (int64_t i = 0; i < N; ++i) {
         double s = lco_dot(qb, keys + i * (int64_t)d, d);
-        if (s > best) {
+        if (better(s, best)) {
             second = best;
             best = s;
             bi = i;
@@ -427,5 +436,89 @@ void lco_accept_length(const void *logits, int32_t dtype, int32_t V, const int32
         while (len < k && p_target[(int64_t)b * k + len] >= (double)p_draft[(int64_t)b * k + len])
             ++len;
         accept_len[b] = len;
+    }
+}
+
+/*
+ * Locality-sensitive index for stage 1 (Section 3, Eq. (1): the cache key is an
+ * LSH h(z) of the embedding, with collision probability above p1 for close
+ * pairs and below p2 for far ones; Algorithm 1 searches the cache with it).
+ * For cosine distance the hash family is random hyperplanes: bit i of h(z) is
+ * 1 when r_i . z >= 0 (the hyperplanes r_i are inputs, bfloat16 [bits][d]),
+ * so two vectors at angle theta agree on a bit with probability 1 - theta/pi.
+ * z is the stored (normalised, bfloat16-rounded) vector.  Bits are packed 32
+ * to a word, bit i in word i / 32 at position i % 32.
+ *
+ * lco_simhash: sig [n][bits/32], proj [n][bits] (the projections, in double).
+ */
+void lco_simhash(const uint16_t *z, int64_t n, int32_t d, const uint16_t *r, int32_t bits, uint32_t *sig,
+                 double *proj)
+{
+    const int32_t words = bits / 32;
+#pragma omp parallel for schedule(static)
+    for (int64_t j = 0; j < n; ++j) {
+        for (int32_t w = 0; w < words; ++w)
+            sig[j * words + w] = 0u;
+        for (int32_t i = 0; i < bits; ++i) {
+            double p = lco_dot(r + (int64_t)i * d, z + j * (int64_t)d, d);
+            proj[j * (int64_t)bits + i] = p;
+            if (p >= 0.0)
+                sig[j * words + i / 32] |= 1u << (i % 32);
+        }
+    }
+}
+
+/* Number of differing bits of two signatures of `words` words. */
+static int32_t hamming(const uint32_t *a, const uint32_t *b, int32_t words)
+{
+    int32_t h = 0;
+    for (int32_t w = 0; w < words; ++w)
+        h += __builtin_popcount(a[w] ^ b[w]);
+    return h;
+}
+
+/*
+ * The lookup with the LSH index as stage 1: the candidates of a query are the
+ * entries whose signature differs from the query's in at most `radius` bits
+ * (radius 0: equal hash keys, as in Algorithm 1; radius = bits: every entry).
+ * Among the candidates the entry of highest exact similarity (lowest index on
+ * ties) is the stage-1 result; then the threshold and stage 2 as in
+ * lco_lookup.  No candidate: idx -1, score NaN, MISS.  n_cand[b] receives the
+ * candidate count.
+ */
+void lco_lookup_lsh(const uint16_t *keys, const uint16_t *emb, const int32_t *tokens, const uint32_t *sig_keys,
+                    int64_t N, int32_t d, int32_t k_cap, int32_t bits, const uint16_t *q, const uint32_t *sig_q,
+                    const uint16_t *a, const int32_t *u, int32_t B, int32_t radius, float tau_q, float tau_r,
+                    int32_t k, int32_t *idx, float *score, float *resp_score, int32_t *decision, int32_t *n_cand)
+{
+    const int32_t words = bits / 32;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int32_t b = 0; b < B; ++b) {
+        const uint16_t *qb = q + (int64_t)b * d;
+        double best = -INFINITY;
+        int64_t bi = -1;
+        int32_t cnt = 0;
+        for (int64_t i = 0; i < N; ++i) {
+            if (hamming(sig_q + (int64_t)b * words, sig_keys + i * words, words) > radius)
+                continue;
+            ++cnt;
+            double s = lco_dot(qb, keys + i * (int64_t)d, d);
+            if (better(s, best)) {
+                best = s;
+                bi = i;
+            }
+        }
+        n_cand[b] = cnt;
+        if (bi < 0) {
+            idx[b] = -1;
+            score[b] = quiet_nan();
+            resp_score[b] = quiet_nan();
+            decision[b] = LCO_MISS;
+            continue;
+        }
+        idx[b] = (int32_t)bi;
+        double s;
+        decision[b] = decide_one(keys, emb, tokens, d, k_cap, qb, a + (int64_t)b * d, u + (int64_t)b * k, tau_q,
+                                 tau_r, k, bi, &s, &score[b], &resp_score[b]);
     }
 }

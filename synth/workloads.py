@@ -430,6 +430,15 @@ def draft_verification(B: int, k: int, V: int, seed: int, in_dtype: int = BF16, 
     return logits.reshape(B, k, V), tokens.reshape(B, k), p_draft.reshape(B, k)
 
 
+_S_HYP = 80
+
+
+def hyperplanes(bits: int, d: int, seed: int) -> np.ndarray:
+    """Random hyperplanes of a locality-sensitive index for cosine distance: [bits][d] N(0, 1) entries as
+    bfloat16 bit patterns (uint16).  They are the random numbers the index draws, passed in as an input."""
+    return to_bf16_bits(_rng(seed, _S_HYP).standard_normal((bits, d), dtype=np.float32))
+
+
 def generate(sp: Spec | str, threads: int | None = None, **overrides) -> Workload:
     """Build the cache contents and one batch of queries for a spec."""
     if isinstance(sp, str):
@@ -448,4 +457,4 @@ def generate(sp: Spec | str, threads: int | None = None, **overrides) -> Workloa
 __all__ = ["Spec", "Workload", "CONFIGS", "spec", "generate", "entries", "queries", "to_bf16_bits",
            "bf16_bits_to_f64", "as_f64", "CLS_MISS", "CLS_BENIGN", "CLS_COLLISION",
            "F32", "BF16", "GEN_CHUNK", "SERVE_SMALL_CALL_B", "ENSEMBLE_DIMS", "ensemble_entries",
-           "ensemble_lookahead", "calibration_pairs", "draft_verification"]
+           "ensemble_lookahead", "calibration_pairs", "draft_verification", "hyperplanes"]

@@ -11,7 +11,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 SRC = os.path.join(ROOT, "oracle", "lacache_oracle.c")
 
 MUTANTS = {
-    "ties go to the highest index": ("if (s > best) {", "if (s >= best) {"),
+    "ties go to the highest index": ("return s > best;", "return s >= best;"),
     "dot product drops its last term": ("for (int32_t j = 0; j < d; ++j)\n        s += widen_bf16",
                                         "for (int32_t j = 0; j < d - 1; ++j)\n        s += widen_bf16"),
     "dot product subtracts": ("s += widen_bf16(x[j]) * widen_bf16(y[j]);", "s -= widen_bf16(x[j]) * widen_bf16(y[j]);"),
@@ -49,6 +49,10 @@ MUTANTS = {
         "            len += p_target[(int64_t)b * k + j] >= (double)p_draft[(int64_t)b * k + j];"),
     "softmax without the max shift": ("s += exp(read_in(logits, dtype, row, V, v) - m);",
                                       "s += exp(read_in(logits, dtype, row, V, v));"),
+    "hyperplane bit set only on a strictly positive projection": ("if (p >= 0.0)\n                sig[j * words",
+                                                                   "if (p > 0.0)\n                sig[j * words"),
+    "candidates strictly inside the radius": ("words) > radius)", "words) >= radius)"),
+    "Hamming distance from OR instead of XOR": ("__builtin_popcount(a[w] ^ b[w])", "__builtin_popcount(a[w] | b[w])"),
     "probability read at the next vocabulary entry": ("exp(read_in(logits, dtype, row, V, t) - m) / s",
                                                       "exp(read_in(logits, dtype, row, V, (t + 1) % V) - m) / s"),
 }

@@ -633,3 +633,96 @@ def test_accept_length_invariances():
         cur = oracle.accept_length(lg, oracle.F32, tok, (pd * f).astype(np.float32))["accept_len"]
         assert np.all(cur <= prev)
         prev = cur
+
+
+# --------------------------------------------------------------------------- LSH index for stage 1 (Eq. (1))
+
+
+def test_simhash_is_the_sign_of_the_projections():
+    rng = np.random.default_rng(81)
+    n, d, bits = 300, 48, 96
+    z = oracle.quantise(rng.standard_normal((n, d)).astype(np.float32), oracle.F32)
+    z[5] = 0                                                   # zero vector: every projection is 0 -> all bits 1
+    r = synth.hyperplanes(bits, d, seed=3)
+    sig, proj = oracle.simhash(z, r, bits)
+    P = bf.widen(z) @ bf.widen(r).T
+    np.testing.assert_allclose(proj, P, rtol=0, atol=1e-12)
+    want = np.zeros((n, bits // 32), np.uint32)
+    for i in range(bits):
+        want[:, i // 32] |= (P[:, i] >= 0).astype(np.uint32) << np.uint32(i % 32)
+    np.testing.assert_array_equal(sig, want)
+    assert np.all(sig[5] == 0xFFFFFFFF)
+
+
+def test_simhash_collision_probability_is_one_minus_angle_over_pi():
+    """Random hyperplanes: two vectors at angle theta agree on a bit with probability 1 - theta/pi
+    (the gapped collision property of Eq. (1) for cosine distance)."""
+    rng = np.random.default_rng(82)
+    d, bits = 64, 8192
+    r = synth.hyperplanes(bits, d, seed=4)
+    x = rng.standard_normal(d)
+    x /= np.linalg.norm(x)
+    v = rng.standard_normal(d)
+    v -= (v @ x) * x
+    v /= np.linalg.norm(v)
+    for theta in (0.1, 0.5, 1.0, np.pi / 2, 2.5):
+        y = np.cos(theta) * x + np.sin(theta) * v
+        z = oracle.quantise(np.stack([x, y]).astype(np.float32), oracle.F32)
+        sig, _ = oracle.simhash(z, r, bits)
+        agree = bits - sum(bin(int(w)).count("1") for w in (sig[0] ^ sig[1]))
+        ang = np.arccos(np.clip(bf.widen(z[0]) @ bf.widen(z[1]), -1, 1))
+        p = 1 - ang / np.pi
+        assert abs(agree / bits - p) <= 4 * np.sqrt(p * (1 - p) / bits) + 1e-3, (theta, agree / bits, p)
+
+
+def _lsh_case(rng, N=600, d=40, bits=64, B=50):
+    keys, emb, tok = _store(rng, N, d, k_cap=6, vocab=20)
+    q = keys[rng.integers(0, N, B)].copy()
+    noise = oracle.quantise(rng.standard_normal((B, d)).astype(np.float32), oracle.F32)
+    mix = (0.9 * bf.widen(q) + 0.3 * bf.widen(noise)).astype(np.float32)
+    q = oracle.quantise(mix, oracle.F32)
+    q[:5] = keys[:5]                                           # self queries
+    a = oracle.quantise(rng.standard_normal((B, d)).astype(np.float32), oracle.F32)
+    u = rng.integers(0, 20, (B, 6), dtype=np.int32)
+    r = synth.hyperplanes(bits, d, seed=int(rng.integers(1 << 30)))
+    sk, _ = oracle.simhash(keys, r, bits)
+    sq, _ = oracle.simhash(q, r, bits)
+    return keys, emb, tok, q, a, u, sk, sq, bits
+
+
+def test_lsh_lookup_matches_bruteforce_candidates():
+    rng = np.random.default_rng(83)
+    keys, emb, tok, q, a, u, sk, sq, bits = _lsh_case(rng)
+    S = bf.scores(q, keys)
+    H = np.array([[sum(bin(int(w)).count("1") for w in (sq[b] ^ sk[i])) for i in range(len(keys))]
+                  for b in range(len(q))])
+    for radius in (0, 3, 10, 20, bits):
+        o = oracle.lookup_lsh(keys, emb, tok, sk, q, sq, a, u, radius, 0.5, 0.6, 6)
+        cand = H <= radius
+        np.testing.assert_array_equal(o["n_cand"], cand.sum(axis=1))
+        masked = np.where(cand, S, -np.inf)
+        want = np.where(cand.any(axis=1), np.argmax(masked, axis=1), -1)
+        np.testing.assert_array_equal(o["idx"], want)
+        full = o["idx"] >= 0
+        np.testing.assert_allclose(o["score"][full], np.clip(S[full, want[full]], -1, 1).astype(np.float32),
+                                   rtol=0, atol=1e-6)
+        assert np.all(np.isnan(o["score"][~full])) and np.all(o["decision"][~full] == oracle.MISS)
+        assert np.all(o["idx"][:5] == np.arange(5)) or radius < 0      # a self query is always a candidate
+    # radius = bits: every entry is a candidate, so the LSH lookup is the exact lookup
+    e = oracle.lookup(keys, emb, tok, q, a, u, 0.5, 0.6, 6)
+    o = oracle.lookup_lsh(keys, emb, tok, sk, q, sq, a, u, bits, 0.5, 0.6, 6)
+    for f in ("idx", "score", "decision"):
+        np.testing.assert_array_equal(o[f], e[f])
+    np.testing.assert_array_equal(np.isnan(o["resp_score"]), np.isnan(e["resp_score"]))
+
+
+def test_lsh_radius_monotone():
+    rng = np.random.default_rng(84)
+    keys, emb, tok, q, a, u, sk, sq, bits = _lsh_case(rng)
+    prev_n, prev_s = None, None
+    for radius in range(0, bits + 1, 4):
+        o = oracle.lookup_lsh(keys, emb, tok, sk, q, sq, a, u, radius, 0.5, 0.6, 6)
+        s = np.where(o["idx"] >= 0, o["score"], -np.inf)
+        if prev_n is not None:
+            assert np.all(o["n_cand"] >= prev_n) and np.all(s >= prev_s)
+        prev_n, prev_s = o["n_cand"], s
