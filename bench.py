@@ -13,7 +13,8 @@ regime) is measured in the same run and reported under "secondary", and the
 same keys with the four-model lookahead ensemble (Section 4.4) under
 "ensemble", threshold calibration over a million benign pairs
 (Appendix A.2) under "calibration", and the speculative-decoding acceptance
-of 256 x 20 draft tokens (Section 4.3) under "accept".  For
+of 256 x 20 draft tokens (Section 4.3) under "accept", and the serve_small
+lookup with stage 1 through the LSH index (Eq. (1)) under "lsh".  For
 each, "roofline" rates the stage-1 kernel, timed with HIP events recorded by
 the library on the launch stream, against the MI355X peak (bf16 dense MFMA
 2.5 PFLOP/s, HBM 8 TB/s).  "cpu_baseline" times the CPU oracle on a bounded
@@ -50,6 +51,7 @@ def parse():
     ap.add_argument("--no-ensemble", action="store_true", help="skip the lookahead-ensemble measurement")
     ap.add_argument("--no-calibration", action="store_true", help="skip the threshold-calibration measurement")
     ap.add_argument("--no-accept", action="store_true", help="skip the speculative-decoding acceptance measurement")
+    ap.add_argument("--no-lsh", action="store_true", help="skip the LSH-indexed lookup measurement")
     ap.add_argument("--no-probe", action="store_true",
                     help="skip the attainable-ceiling probe (sustained MFMA rate on random bf16, HBM streaming read)")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
@@ -339,6 +341,66 @@ def run_accept(steps, warmup, lc, torch, synth):
                 logits_read_gbs=logit_bytes / (ms * 1e-3) / 1e9)
 
 
+def run_lsh(steps, warmup, lc, torch, synth):
+    """The serve_small workload (1M x 768 keys, 16 queries per call) with stage 1 through the LSH index
+    (Eq. (1)): 256 random-hyperplane bits per entry, candidates within 64 differing bits, exact re-rank.
+    One step is one lacache_lookup_lsh call; recall is measured over the whole 4096-query pool against the
+    exact lookup of the same pool."""
+    from tests.gpu_util import gpu_cache, to_dev
+    sp = synth.spec("serve_small")
+    call_b, bits, radius = synth.SERVE_SMALL_CALL_B, 256, 64
+    t0 = time.time()
+    w = synth.generate(sp)
+    log(f"[bench] lsh: generated in {time.time() - t0:.1f}s")
+    c = gpu_cache(lc, sp, w.keys, w.emb, w.tokens, max_batch=sp.B, insert_chunk=1 << 18)
+    q, a = to_dev(w.queries), to_dev(w.la_emb)
+    t = to_dev(np.ascontiguousarray(w.la_tok[:, :sp.k]))
+    exact = c.lookup(q, a, t, sp.tau_q, sp.tau_r, sp.k)
+    torch.cuda.synchronize()
+    ex_idx, ex_dec = exact[0].cpu().numpy(), exact[3].cpu().numpy()
+    t0 = time.time()
+    c.enable_lsh(bits, to_dev(synth.hyperplanes(bits, sp.d, seed=sp.seed + 1000)), 256)
+    torch.cuda.synchronize()
+    t_index = time.time() - t0
+    n_calls = sp.B // call_b
+    dev = torch.device("cuda", 0)
+    outs = [tuple(torch.empty(call_b, dtype=dt, device=dev)
+                  for dt in (torch.int32, torch.float32, torch.float32, torch.int32, torch.int32))
+            for _ in range(n_calls)]
+
+    def step(i):
+        j = i % n_calls
+        sl = slice(j * call_b, (j + 1) * call_b)
+        c.lookup_lsh(q[sl], a[sl], t[sl], sp.tau_q, sp.tau_r, sp.k, radius, out=outs[j])
+
+    for i in range(warmup):
+        step(i)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(steps):
+        step(i)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    for i in range(n_calls):
+        step(i)
+    torch.cuda.synchronize()
+    idx = np.concatenate([o[0].cpu().numpy() for o in outs])
+    dec = np.concatenate([o[3].cpu().numpy() for o in outs])
+    nc = np.concatenate([o[4].cpu().numpy() for o in outs])
+    hit = ex_dec >= 1
+    c.close()
+    del w, q, a, t
+    torch.cuda.empty_cache()
+    return dict(workload=f"serve_small keys (1M x 768), {call_b} queries per call, {bits}-bit random-hyperplane "
+                         f"signatures, Hamming radius {radius}, exact re-rank",
+                value=call_b / (ms * 1e-3), unit="lookups/s", ms_per_step=ms,
+                recall_stage1_hits=float(np.mean((idx == ex_idx) & (dec == ex_dec), where=hit)),
+                decisions_equal=float(np.mean(dec == ex_dec)), mean_candidates=float(nc.mean()),
+                signature_bytes=float(sp.N) * bits / 8, index_build_s=t_index)
+
+
 def cpu_baseline(sp, w, call_b):
     """The CPU oracle, as it is, on a bounded sample: a few queries against the full cache."""
     import oracle
@@ -389,6 +451,7 @@ def main():
     ensemble = None if args.no_ensemble else run_ensemble(args.steps, args.warmup, lc, torch, synth)
     calibration = None if args.no_calibration else run_calibration(args.steps, args.warmup, lc, torch, synth)
     accept = None if args.no_accept else run_accept(args.steps, args.warmup, lc, torch, synth)
+    lsh = None if args.no_lsh else run_lsh(args.steps, args.warmup, lc, torch, synth)
 
     line = {
         "metric": "cache lookups/sec (2-stage) at N=1M,d=768; % HBM / MFMA roofline",
@@ -422,6 +485,8 @@ def main():
         line["calibration"] = calibration
     if accept:
         line["accept"] = accept
+    if lsh:
+        line["lsh"] = lsh
     if probe:
         # the same kernels rated against what this GPU sustains: MFMA throughput on random bf16 operands
         # (operand-dependent power lowers the clock below the datasheet's) and a plain streaming read

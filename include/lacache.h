@@ -225,6 +225,43 @@ int lacache_accept_length(const void *logits, lacache_dtype dtype, int32_t V, co
                           void *stream);
 
 /*
+ * Locality-sensitive index for stage 1 (Section 3, Eq. (1): the cache key is
+ * an LSH of the embedding, colliding with probability above p1 for close
+ * pairs and below p2 for far ones; Algorithm 1 searches the cache with it).
+ * Random hyperplanes, the LSH family of cosine distance: bit i of a stored or
+ * query vector z (normalised and bfloat16-rounded) is 1 when the projection
+ * r_i . z (bf16 products, float32 sums) is >= 0; bits are packed 32 to a word,
+ * bit i in word i / 32 at position i % 32.
+ *
+ * lacache_enable_lsh: hyperplanes [bits][d] bfloat16 (device; not
+ * normalised; their entries are the random numbers the index draws), bits a
+ * multiple of 32 in 32 .. 256, max_candidates 1 .. 65536 entries kept per
+ * query.  Allocates the index (signatures [capacity][bits / 32] and per-query
+ * candidate lists), waits for `stream`, and computes the signatures of every
+ * stored entry; later inserts add theirs.  Calling it again replaces the index.
+ */
+int lacache_enable_lsh(lacache_t h, int32_t bits, const uint16_t *hyperplanes, int32_t max_candidates, void *stream);
+
+/*
+ * lacache_lookup with the LSH index as stage 1 (caches with one prefix model):
+ * the candidates of a query are the entries whose signature differs from the
+ * query's in at most `radius` bits (0 .. bits; 0 is equality of hash keys,
+ * bits makes every entry a candidate); among them the entry of highest exact
+ * similarity (lowest index on ties) is the stage-1 result, then the
+ * threshold and stage 2 as in lacache_lookup.  With no candidate: idx -1,
+ * score NaN, MISS.  n_cand [B] int32 receives each query's candidate count;
+ * a count above max_candidates means only max_candidates of them (in no
+ * particular order) were ranked.  Other arguments and outputs as in
+ * lacache_lookup.  LACACHE_EINVAL if the index is not enabled.
+ */
+int lacache_lookup_lsh(lacache_t h, const void *queries, const void *lookahead_emb, const int32_t *lookahead_tokens,
+                       int32_t B, float tau_q, float tau_r, int32_t k, int32_t radius, int32_t *idx, float *score,
+                       float *resp_score, int32_t *decision, int32_t *n_cand, void *stream);
+
+/* Copy the LSH signatures of entries first .. first+n-1 ([n][bits / 32] uint32, device) out. */
+int lacache_export_signatures(lacache_t h, int64_t first, int32_t n, uint32_t *sig, void *stream);
+
+/*
  * Batch-size crossover of stage 1: batches of at most b_small queries use the
  * bandwidth-bound streaming kernel, larger ones the matrix-core GEMM kernel.
  * 0 <= b_small <= 64 (default 64; 0 sends every batch to the GEMM kernel).

@@ -38,6 +38,9 @@ _lib.lacache_lookup_ensemble.argtypes = [_P, _P, ctypes.POINTER(_P), _P, _i32, _
 _lib.lacache_export_prefix.argtypes = [_P, _i32, _i64, _i32, _P, _P]
 _lib.lacache_calibrate.argtypes = [_P, _i32, _P, _P, _i64, _f32, _f32, _P, _P, _P]
 _lib.lacache_accept_length.argtypes = [_P, ctypes.c_int, _i32, _P, _P, _i32, _i32, _P, _P, _P]
+_lib.lacache_enable_lsh.argtypes = [_P, _i32, _P, _i32, _P]
+_lib.lacache_lookup_lsh.argtypes = [_P, _P, _P, _P, _i32, _f32, _f32, _i32, _i32, _P, _P, _P, _P, _P, _P]
+_lib.lacache_export_signatures.argtypes = [_P, _i64, _i32, _P, _P]
 _lib.lacache_destroy.argtypes = [_P]
 _lib.lacache_insert.argtypes = [_P, _P, _P, _P, _i32, ctypes.POINTER(_i64), _P]
 _lib.lacache_lookup.argtypes = [_P, _P, _P, _P, _i32, _f32, _f32, _i32, _P, _P, _P, _P, _P]
@@ -53,6 +56,7 @@ _lib.lacache_strerror.restype = ctypes.c_char_p
 EXPORTED = ("lacache_create", "lacache_create_ensemble", "lacache_models", "lacache_destroy", "lacache_insert",
             "lacache_insert_ensemble", "lacache_lookup", "lacache_lookup_ensemble", "lacache_size",
             "lacache_export", "lacache_export_prefix", "lacache_calibrate", "lacache_accept_length",
+            "lacache_enable_lsh", "lacache_lookup_lsh", "lacache_export_signatures",
             "lacache_set_small_batch",
             "lacache_profile", "lacache_profile_read", "lacache_strerror")
 
@@ -144,6 +148,16 @@ class LaCache:
 
     def export_prefix(self, model: int, first: int, n: int, stream=None):
         return lacache_export_prefix(self, model, first, n, stream)
+
+    def enable_lsh(self, bits: int, hyperplanes, max_candidates: int = 256, stream=None) -> None:
+        lacache_enable_lsh(self, bits, hyperplanes, max_candidates, stream)
+
+    def lookup_lsh(self, queries, lookahead_emb, lookahead_tokens, tau_q, tau_r, k, radius, out=None, stream=None):
+        return lacache_lookup_lsh(self, queries, lookahead_emb, lookahead_tokens, tau_q, tau_r, k, radius, out,
+                                  stream)
+
+    def export_signatures(self, first: int, n: int, stream=None):
+        return lacache_export_signatures(self, first, n, stream)
 
     def calibrate(self, a, b, percentile: float, cap: float, which: int = -1, out=None, stream=None):
         return lacache_calibrate(self, which, a, b, percentile, cap, out, stream)
@@ -331,6 +345,46 @@ def lacache_accept_length(logits, draft_tokens, p_draft, out=None, stream=None):
                                       acc.data_ptr(), pt.data_ptr(), _stream(dev.index, stream)),
            "lacache_accept_length")
     return out
+
+
+def lacache_enable_lsh(c: LaCache, bits: int, hyperplanes, max_candidates: int = 256, stream=None) -> None:
+    """hyperplanes: [bits][d] bfloat16 (or int16/uint16 bits) on the cache's device."""
+    hp = _vec(hyperplanes, BF16, bits, c.d, c.device, "hyperplanes")
+    _check(_lib.lacache_enable_lsh(c.handle, int(bits), hp, int(max_candidates), _stream(c.device, stream)),
+           "lacache_enable_lsh")
+    c.lsh_bits = int(bits)
+
+
+def lacache_lookup_lsh(c: LaCache, queries, lookahead_emb, lookahead_tokens, tau_q: float, tau_r: float, k: int,
+                       radius: int, out=None, stream=None):
+    """Returns (idx int32, score f32, resp_score f32, decision int32, n_cand int32), each [B]."""
+    B = queries.shape[0]
+    dev = torch.device("cuda", c.device)
+    if out is None:
+        out = (torch.empty(B, dtype=torch.int32, device=dev), torch.empty(B, dtype=torch.float32, device=dev),
+               torch.empty(B, dtype=torch.float32, device=dev), torch.empty(B, dtype=torch.int32, device=dev),
+               torch.empty(B, dtype=torch.int32, device=dev))
+    for t, dt, nm in zip(out, (torch.int32, torch.float32, torch.float32, torch.int32, torch.int32),
+                         ("idx", "score", "resp", "decision", "n_cand")):
+        if t.dtype != dt or t.device != dev or t.numel() != B or not t.is_contiguous():
+            raise ValueError(f"{nm}: expected a contiguous [{B}] {dt} tensor on {dev}")
+    _check(_lib.lacache_lookup_lsh(c.handle, _vec(queries, c.in_dtype, B, c.d, c.device, "queries"),
+                                   _vec(lookahead_emb, c.in_dtype, B, c.d, c.device, "lookahead_emb"),
+                                   _ints(lookahead_tokens, (B, k), c.device, "lookahead_tokens"), B, float(tau_q),
+                                   float(tau_r), int(k), int(radius), *(t.data_ptr() for t in out),
+                                   _stream(c.device, stream)), "lacache_lookup_lsh")
+    return out
+
+
+def lacache_export_signatures(c: LaCache, first: int, n: int, stream=None):
+    """The stored LSH signatures as int32 bit patterns [n][bits / 32] (view as uint32 on the host)."""
+    bits = getattr(c, "lsh_bits", 0)
+    if not bits:
+        raise ValueError("the LSH index is not enabled")
+    sig = torch.empty((n, bits // 32), dtype=torch.int32, device=torch.device("cuda", c.device))
+    _check(_lib.lacache_export_signatures(c.handle, first, n, sig.data_ptr(), _stream(c.device, stream)),
+           "lacache_export_signatures")
+    return sig
 
 
 def lacache_set_small_batch(c: LaCache, b_small: int) -> None:

@@ -15,7 +15,7 @@ CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "liblacache.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
 SOURCES = ["lacache.cpp", "k_store.hip", "k_stage1_stream.hip", "k_stage1_gemm.hip", "k_verify.hip",
-           "k_calibrate.hip", "k_accept.hip"]
+           "k_calibrate.hip", "k_accept.hip", "k_lsh.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 FLAGS = [

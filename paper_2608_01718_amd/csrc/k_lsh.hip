@@ -1,0 +1,164 @@
+// k_lsh.hip -- stage 1 through a locality-sensitive index: random-hyperplane signatures, a Hamming-radius
+// candidate scan, and exact re-ranking of the candidates.
+//
+// Section 3 models the cache key as an LSH h(z) of the embedding with the
+// gapped collision property of Eq. (1), and Algorithm 1 searches the cache
+// with it.  For cosine distance the hash family is random hyperplanes: bit i
+// of h(z) is 1 when r_i . z >= 0, so vectors at angle theta agree on a bit
+// with probability 1 - theta / pi.  Signatures of the stored (normalised,
+// bfloat16-rounded) keys are kept beside the store; a query's candidates are
+// the entries within a Hamming radius of its signature (radius 0 is equality
+// of hash keys), found by one pass over the signatures (bits / 8 bytes per
+// entry instead of the key's d * 2), and re-ranked by their exact similarity.
+#include "common.hpp"
+#include "launch.hpp"
+
+namespace lacache {
+
+namespace {
+constexpr int kScanQueries = 1024;  // query signatures held in LDS per scan launch
+}
+
+// Copy a row-major [rows][d] bfloat16 matrix into the tiled layout with d_pad columns (zero padded), as is.
+__global__ __launch_bounds__(256) void k_tile_rows(const uint16_t* __restrict__ src, int rows, int d, int d_pad,
+                                                   uint16_t* __restrict__ dst) {
+    const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (t >= (int64_t)rows * d_pad) return;
+    const int r = (int)(t / d_pad), c = (int)(t - (int64_t)r * d_pad);
+    dst[tiled_offset(r, c, d_pad >> 5)] = c < d ? src[(int64_t)r * d + c] : (uint16_t)0;
+}
+
+// One wave per 16-row group of a tiled matrix: the projections of its rows on every hyperplane (16 at a time,
+// v_mfma_f32_16x16x32_bf16 with the rows as the row operand), packed into sign bits.  Lane l holds, for
+// hyperplane 16 hg + l % 16, the rows 4 (l / 16) + j (j = 0..3); a ballot per j gathers the 16 bits of each
+// row.  Rows outside [row0, row0 + n) are not written.
+__global__ __launch_bounds__(256) void k_simhash(const u32x4* __restrict__ rows_tiled, int kc, int64_t row0,
+                                                 int64_t n, const u32x4* __restrict__ hp_tiled, int bits,
+                                                 uint32_t* __restrict__ sig) {
+    const int lane = threadIdx.x & 63;
+    const int64_t g = (row0 >> 4) + (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);  // 16-row group
+    if (g * 16 >= row0 + n) return;
+    const int words = bits >> 5;
+    const u32x4* a = rows_tiled + g * kc * 64 + lane;
+    uint32_t word = 0u;
+    for (int hg = 0; hg < (bits >> 4); ++hg) {
+        f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+        const u32x4* b = hp_tiled + (int64_t)hg * kc * 64 + lane;
+        for (int c = 0; c < kc; ++c) acc = mfma16x16x32(a[c * 64], b[c * 64], acc);
+        uint64_t m[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) m[j] = __ballot(acc[j] >= 0.0f);
+        // lane l < 16 owns row 4 (l / 4) + l % 4 = l of the group: its bits sit in m[l % 4] at 16 (l / 4)
+        const uint64_t mine = (lane & 3) == 0 ? m[0] : (lane & 3) == 1 ? m[1] : (lane & 3) == 2 ? m[2] : m[3];
+        const uint32_t b16 = (uint32_t)(mine >> (16 * ((lane >> 2) & 3))) & 0xFFFFu;
+        word |= b16 << (16 * (hg & 1));
+        if (hg & 1) {
+            const int64_t row = g * 16 + lane;
+            if (lane < 16 && row >= row0 && row < row0 + n) sig[row * words + (hg >> 1)] = word;
+            word = 0u;
+        }
+    }
+}
+
+__global__ __launch_bounds__(256) void k_lsh_clear(uint32_t* __restrict__ cnt, int B) {
+    const int i = blockIdx.x * 256 + threadIdx.x;
+    if (i < B) cnt[i] = 0u;
+}
+
+// Candidates of queries q0 .. q0+nq-1: every entry whose signature differs from the query's in at most `radius`
+// bits is appended to the query's list (at most max_cand kept; cnt counts them all).  One thread per entry,
+// the query signatures in LDS.
+__global__ __launch_bounds__(256) void k_lsh_scan(const uint32_t* __restrict__ sig_keys, int64_t n_rows,
+                                                  const uint32_t* __restrict__ sig_q, int q0, int nq, int words,
+                                                  int radius, int max_cand, uint32_t* __restrict__ cnt,
+                                                  int32_t* __restrict__ cand) {
+    __shared__ uint32_t sq[kScanQueries * 8];
+    for (int i = threadIdx.x; i < nq * words; i += 256) sq[i] = sig_q[(int64_t)q0 * words + i];
+    __syncthreads();
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n_rows; i += (int64_t)gridDim.x * 256) {
+        uint32_t k[8];
+#pragma unroll
+        for (int w = 0; w < 8; ++w) k[w] = w < words ? sig_keys[i * words + w] : 0u;
+        for (int b = 0; b < nq; ++b) {
+            int h = 0;
+#pragma unroll
+            for (int w = 0; w < 8; ++w)
+                if (w < words) h += __popc(k[w] ^ sq[b * words + w]);
+            if (h <= radius) {
+                const uint32_t pos = atomicAdd(&cnt[q0 + b], 1u);
+                if (pos < (uint32_t)max_cand) cand[(int64_t)(q0 + b) * max_cand + pos] = (int32_t)i;
+            }
+        }
+    }
+}
+
+// One wave per query: the exact similarity of each candidate (the query and the entry read from their tiled
+// stores, bf16 products summed in float32), the best as a packed top-1 (order-free: highest score, lowest
+// index), written as the query's single stage-1 partial; n_cand receives the candidate count.
+__global__ __launch_bounds__(256) void k_lsh_rerank(const u32x4* __restrict__ keys_tiled,
+                                                    const u32x4* __restrict__ qt, int kc, int B,
+                                                    const uint32_t* __restrict__ cnt,
+                                                    const int32_t* __restrict__ cand, int max_cand,
+                                                    uint64_t* __restrict__ part, int32_t* __restrict__ n_cand) {
+    const int lane = threadIdx.x & 63;
+    const int b = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (b >= B) return;
+    const uint32_t c_all = cnt[b];
+    const int nc = c_all < (uint32_t)max_cand ? (int)c_all : max_cand;
+    const int d_pad = kc * 32;
+    uint64_t best = 0ull;
+    for (int t = 0; t < nc; ++t) {
+        const int32_t i = cand[(int64_t)b * max_cand + t];
+        float acc = 0.0f;
+        for (int j0 = lane * 8; j0 < d_pad; j0 += 512) {
+            const u32x4 kv = *(const u32x4*)((const uint16_t*)keys_tiled + tiled_offset(i, j0, kc));
+            const u32x4 qv = *(const u32x4*)((const uint16_t*)qt + tiled_offset(b, j0, kc));
+            acc = dot8_bf16(qv, kv, acc);
+        }
+        acc = wave_sum_f32(acc);
+        best = umax64(best, pack_top1(acc, i));
+    }
+    if (lane == 0) {
+        part[b] = best;
+        n_cand[b] = (int32_t)c_all;
+    }
+}
+
+hipError_t launch_tile_rows(const uint16_t* src, int rows, int d, int d_pad, uint16_t* dst, hipStream_t s) {
+    const int64_t total = (int64_t)rows * d_pad;
+    if (total <= 0) return hipSuccess;
+    k_tile_rows<<<dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s>>>(src, rows, d, d_pad, dst);
+    return hipGetLastError();
+}
+
+hipError_t launch_simhash(const uint16_t* rows_tiled, int d_pad, int64_t row0, int64_t n, const uint16_t* hp_tiled,
+                          int bits, uint32_t* sig, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    const int64_t g0 = row0 >> 4, g1 = (row0 + n + 15) >> 4;
+    k_simhash<<<dim3((unsigned)((g1 - g0 + 3) / 4)), dim3(256), 0, s>>>(
+        (const u32x4*)rows_tiled, d_pad >> 5, row0, n, (const u32x4*)hp_tiled, bits, sig);
+    return hipGetLastError();
+}
+
+hipError_t launch_lsh_stage1(const uint16_t* keys_tiled, const uint32_t* sig_keys, int64_t n_rows,
+                             const uint16_t* qt, const uint32_t* sig_q, int B, int d_pad, int bits, int radius,
+                             int max_cand, uint32_t* cnt, int32_t* cand, uint64_t* part, int32_t* n_cand,
+                             int num_cu, hipStream_t s) {
+    if (B <= 0) return hipSuccess;
+    const int words = bits >> 5;
+    if (words < 1 || words > 8) return hipErrorInvalidValue;
+    k_lsh_clear<<<dim3((unsigned)((B + 255) / 256)), dim3(256), 0, s>>>(cnt, B);
+    int64_t blocks = (n_rows + 255) / 256;
+    if (blocks > 8 * num_cu) blocks = 8 * num_cu;
+    if (blocks < 1) blocks = 1;
+    for (int q0 = 0; q0 < B && n_rows > 0; q0 += kScanQueries) {
+        const int nq = B - q0 < kScanQueries ? B - q0 : kScanQueries;
+        k_lsh_scan<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(sig_keys, n_rows, sig_q, q0, nq, words, radius,
+                                                               max_cand, cnt, cand);
+    }
+    k_lsh_rerank<<<dim3((unsigned)((B + 3) / 4)), dim3(256), 0, s>>>(
+        (const u32x4*)keys_tiled, (const u32x4*)qt, d_pad >> 5, B, cnt, cand, max_cand, part, n_cand);
+    return hipGetLastError();
+}
+
+}  // namespace lacache

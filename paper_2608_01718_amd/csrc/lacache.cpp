@@ -30,6 +30,13 @@ struct lacache_s {
     uint16_t* qt = nullptr;    // tiled [mb_pad][d_pad] normalised queries
     uint64_t* part = nullptr;  // [max_batch][kMaxPartials] packed top-1 candidates
     uint32_t* calib = nullptr; // [kCalibScratchWords] state and histograms of the calibration select
+    // LSH index (lacache_enable_lsh): hyperplanes, key and query signatures, candidate lists
+    int lsh_bits = 0, lsh_max_cand = 0;
+    uint16_t* hp = nullptr;        // tiled [lsh_bits][d_pad] raw hyperplanes
+    uint32_t* sig = nullptr;       // [cap][lsh_bits / 32]
+    uint32_t* sigq = nullptr;      // [max_batch][lsh_bits / 32]
+    uint32_t* lsh_cnt = nullptr;   // [max_batch]
+    int32_t* lsh_cand = nullptr;   // [max_batch][lsh_max_cand]
     bool profiling = false;
     std::vector<std::pair<hipEvent_t, hipEvent_t>> prof;
 };
@@ -54,7 +61,20 @@ struct DeviceGuard {
     }
 };
 
+void free_lsh(lacache_s* h) {
+    (void)hipFree(h->hp);
+    (void)hipFree(h->sig);
+    (void)hipFree(h->sigq);
+    (void)hipFree(h->lsh_cnt);
+    (void)hipFree(h->lsh_cand);
+    h->hp = nullptr;
+    h->sig = h->sigq = h->lsh_cnt = nullptr;
+    h->lsh_cand = nullptr;
+    h->lsh_bits = h->lsh_max_cand = 0;
+}
+
 void free_all(lacache_s* h) {
+    free_lsh(h);
     (void)hipFree(h->keys);
     for (int i = 0; i < kMaxModels; ++i) (void)hipFree(h->emb[i]);
     (void)hipFree(h->tokens);
@@ -204,6 +224,8 @@ int lacache_insert_ensemble(lacache_t h, const void* keys, const void* const* re
     if (hipMemcpyAsync(h->tokens + first * h->k_cap, resp_tokens, (size_t)n * h->k_cap * 4,
                        hipMemcpyDeviceToDevice, s) != hipSuccess)
         return LACACHE_EHIP;
+    if (h->lsh_bits && launch_simhash(h->keys, h->d_pad, first, n, h->hp, h->lsh_bits, h->sig, s) != hipSuccess)
+        return LACACHE_EHIP;
     h->size += n;
     if (first_idx) *first_idx = first;
     return LACACHE_OK;
@@ -336,6 +358,86 @@ int lacache_accept_length(const void* logits, lacache_dtype dtype, int32_t V, co
     if (!logits || !draft_tokens || !p_draft || !accept_len || !p_target) return LACACHE_EINVAL;
     if (launch_accept_length(logits, (int)dtype, V, draft_tokens, p_draft, B, k, accept_len, p_target,
                              (hipStream_t)stream) != hipSuccess)
+        return LACACHE_EHIP;
+    return LACACHE_OK;
+}
+
+int lacache_enable_lsh(lacache_t h, int32_t bits, const uint16_t* hyperplanes, int32_t max_candidates,
+                       void* stream) {
+    if (!h || bits < 32 || bits > 256 || bits % 32 != 0 || !hyperplanes || max_candidates < 1 ||
+        max_candidates > 65536)
+        return LACACHE_EINVAL;
+    DeviceGuard g(h->device);
+    if (!g.ok) return LACACHE_EHIP;
+    hipStream_t s = (hipStream_t)stream;
+    // earlier work on the handle may still read the old index
+    if (hipStreamSynchronize(s) != hipSuccess) return LACACHE_EHIP;
+    free_lsh(h);
+    const int words = bits / 32;
+    int rc = LACACHE_OK;
+    if (rc == LACACHE_OK) rc = alloc_zero((void**)&h->hp, (size_t)bits * h->d_pad * 2);
+    if (rc == LACACHE_OK) rc = alloc_zero((void**)&h->sig, (size_t)h->cap * words * 4);
+    if (rc == LACACHE_OK) rc = alloc_zero((void**)&h->sigq, (size_t)h->mb_pad * words * 4);
+    if (rc == LACACHE_OK) rc = alloc_zero((void**)&h->lsh_cnt, (size_t)h->max_batch * 4);
+    if (rc == LACACHE_OK) rc = alloc_zero((void**)&h->lsh_cand, (size_t)h->max_batch * max_candidates * 4);
+    if (rc != LACACHE_OK) {
+        free_lsh(h);
+        return rc;
+    }
+    h->lsh_bits = bits;
+    h->lsh_max_cand = max_candidates;
+    if (launch_tile_rows(hyperplanes, bits, h->d, h->d_pad, h->hp, s) != hipSuccess ||
+        launch_simhash(h->keys, h->d_pad, 0, h->size, h->hp, bits, h->sig, s) != hipSuccess)
+        return LACACHE_EHIP;
+    return LACACHE_OK;
+}
+
+int lacache_lookup_lsh(lacache_t h, const void* queries, const void* lookahead_emb, const int32_t* lookahead_tokens,
+                       int32_t B, float tau_q, float tau_r, int32_t k, int32_t radius, int32_t* idx, float* score,
+                       float* resp_score, int32_t* decision, int32_t* n_cand, void* stream) {
+    if (!h || h->m != 1 || !h->lsh_bits || B < 0 || k < 1 || k > h->k_cap || radius < 0 || radius > h->lsh_bits ||
+        !std::isfinite(tau_q) || !std::isfinite(tau_r))
+        return LACACHE_EINVAL;
+    if (B == 0) return LACACHE_OK;
+    if (!queries || !lookahead_emb || !lookahead_tokens || !idx || !score || !resp_score || !decision || !n_cand)
+        return LACACHE_EINVAL;
+    DeviceGuard g(h->device);
+    if (!g.ok) return LACACHE_EHIP;
+    hipStream_t s = (hipStream_t)stream;
+    const size_t esz = h->dtype == LACACHE_F32 ? 4 : 2;
+    for (int b0 = 0; b0 < B; b0 += h->max_batch) {
+        const int nb = (B - b0) < h->max_batch ? (B - b0) : h->max_batch;
+        const char* q = (const char*)queries + (size_t)b0 * h->d * esz;
+        if (launch_normalise(q, h->dtype, nb, round_up(nb, 16), h->d, h->d_pad, h->qt, 0, true, s) != hipSuccess ||
+            launch_simhash(h->qt, h->d_pad, 0, nb, h->hp, h->lsh_bits, h->sigq, s) != hipSuccess ||
+            launch_lsh_stage1(h->keys, h->sig, h->size, h->qt, h->sigq, nb, h->d_pad, h->lsh_bits, radius,
+                              h->lsh_max_cand, h->lsh_cnt, h->lsh_cand, h->part, n_cand + b0, h->num_cu,
+                              s) != hipSuccess)
+            return LACACHE_EHIP;
+        PrefixModels models{};
+        models.m = 1;
+        models.la[0] = (const char*)lookahead_emb + (size_t)b0 * h->d_resp[0] * esz;
+        models.emb[0] = h->emb[0];
+        models.d[0] = h->d_resp[0];
+        models.d_pad[0] = h->d_pad_resp[0];
+        models.tau[0] = tau_r;
+        if (launch_finalize_verify(h->part, 1, false, h->keys, h->qt, nb, (int)h->size, h->dtype, h->d, models,
+                                   lookahead_tokens + (size_t)b0 * k, k, h->tokens, h->k_cap, tau_q, idx + b0,
+                                   score + b0, resp_score + b0, decision + b0, s) != hipSuccess)
+            return LACACHE_EHIP;
+    }
+    return LACACHE_OK;
+}
+
+int lacache_export_signatures(lacache_t h, int64_t first, int32_t n, uint32_t* sig, void* stream) {
+    if (!h || !h->lsh_bits || first < 0 || n < 0 || first + n > h->size) return LACACHE_EINVAL;
+    if (n == 0) return LACACHE_OK;
+    if (!sig) return LACACHE_EINVAL;
+    DeviceGuard g(h->device);
+    if (!g.ok) return LACACHE_EHIP;
+    const size_t words = (size_t)h->lsh_bits / 32;
+    if (hipMemcpyAsync(sig, h->sig + first * words, (size_t)n * words * 4, hipMemcpyDeviceToDevice,
+                       (hipStream_t)stream) != hipSuccess)
         return LACACHE_EHIP;
     return LACACHE_OK;
 }

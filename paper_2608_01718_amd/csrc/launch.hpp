@@ -61,6 +61,17 @@ hipError_t launch_calibrate(const void* a, const void* b, int dtype, int d, int6
 hipError_t launch_accept_length(const void* logits, int dtype, int V, const int32_t* tokens, const float* p_draft,
                                 int B, int k, int32_t* accept_len, float* p_target, hipStream_t s);
 
+// LSH index (random hyperplanes): tiled copy of the raw hyperplanes, signatures of rows row0 .. row0+n-1 of a
+// tiled matrix ([rows][bits / 32] words, bit i of a row is 1 when its projection on hyperplane i is >= 0),
+// and the stage-1 search (Hamming-radius candidates, exact re-rank) writing one packed partial per query.
+hipError_t launch_tile_rows(const uint16_t* src, int rows, int d, int d_pad, uint16_t* dst, hipStream_t s);
+hipError_t launch_simhash(const uint16_t* rows_tiled, int d_pad, int64_t row0, int64_t n, const uint16_t* hp_tiled,
+                          int bits, uint32_t* sig, hipStream_t s);
+hipError_t launch_lsh_stage1(const uint16_t* keys_tiled, const uint32_t* sig_keys, int64_t n_rows,
+                             const uint16_t* qt, const uint32_t* sig_q, int B, int d_pad, int bits, int radius,
+                             int max_cand, uint32_t* cnt, int32_t* cand, uint64_t* part, int32_t* n_cand,
+                             int num_cu, hipStream_t s);
+
 // Most partials a stage-1 launch may write per query.
 constexpr int kMaxPartials = 1024;
 

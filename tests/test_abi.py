@@ -98,6 +98,14 @@ def test_argument_checks_before_any_device_work(lib):
     assert lib.lacache_accept_length(None, 7, 10, None, None, 1, 1, None, None, None) == EINVAL    # dtype
     assert lib.lacache_accept_length(None, 1, 10, None, None, 1, 1, None, None, None) == EINVAL    # null
     assert lib.lacache_accept_length(None, 1, 10, None, None, 0, 1, None, None, None) == 0         # B = 0
+    lib.lacache_enable_lsh.argtypes = [P, ctypes.c_int32, P, ctypes.c_int32, P]
+    assert lib.lacache_enable_lsh(None, 256, None, 16, None) == EINVAL
+    lib.lacache_lookup_lsh.argtypes = [P] * 5 + [ctypes.c_float, ctypes.c_float, ctypes.c_int32, ctypes.c_int32] + \
+        [P] * 6
+    assert lib.lacache_lookup_lsh(None, None, None, None, 1, 0.5, 0.5, 1, 0, None, None, None, None, None,
+                                  None) == EINVAL
+    lib.lacache_export_signatures.argtypes = [P, ctypes.c_int64, ctypes.c_int32, P, P]
+    assert lib.lacache_export_signatures(None, 0, 0, None, None) == EINVAL
     lib.lacache_strerror.restype = ctypes.c_char_p
     assert lib.lacache_strerror(-2) == b"cache capacity exceeded"
     assert lib.lacache_strerror(12345) == b"unknown error code"
