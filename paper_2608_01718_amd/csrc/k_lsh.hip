@@ -28,35 +28,53 @@ __global__ __launch_bounds__(256) void k_tile_rows(const uint16_t* __restrict__ 
     dst[tiled_offset(r, c, d_pad >> 5)] = c < d ? src[(int64_t)r * d + c] : (uint16_t)0;
 }
 
-// One wave per 16-row group of a tiled matrix: the projections of its rows on every hyperplane (16 at a time,
-// v_mfma_f32_16x16x32_bf16 with the rows as the row operand), packed into sign bits.  Lane l holds, for
+// One wave per (16-row group of a tiled matrix, run of `wpw` signature words): the projections of its rows on
+// the hyperplanes of those words (16 at a time, v_mfma_f32_16x16x32_bf16 with the rows as the row operand; the
+// two 16-hyperplane halves of a word accumulate side by side), packed into sign bits.  Lane l holds, for
 // hyperplane 16 hg + l % 16, the rows 4 (l / 16) + j (j = 0..3); a ballot per j gathers the 16 bits of each
 // row.  Rows outside [row0, row0 + n) are not written.
 __global__ __launch_bounds__(256) void k_simhash(const u32x4* __restrict__ rows_tiled, int kc, int64_t row0,
-                                                 int64_t n, const u32x4* __restrict__ hp_tiled, int bits,
+                                                 int64_t n, const u32x4* __restrict__ hp_tiled, int bits, int wpw,
                                                  uint32_t* __restrict__ sig) {
     const int lane = threadIdx.x & 63;
-    const int64_t g = (row0 >> 4) + (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);  // 16-row group
-    if (g * 16 >= row0 + n) return;
     const int words = bits >> 5;
+    const int chunks = words / wpw;  // word runs per group
+    const int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int64_t g = (row0 >> 4) + wave / chunks;  // 16-row group
+    const int w0 = (int)(wave % chunks) * wpw;
+    if (g * 16 >= row0 + n) return;
     const u32x4* a = rows_tiled + g * kc * 64 + lane;
-    uint32_t word = 0u;
-    for (int hg = 0; hg < (bits >> 4); ++hg) {
-        f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-        const u32x4* b = hp_tiled + (int64_t)hg * kc * 64 + lane;
-        for (int c = 0; c < kc; ++c) acc = mfma16x16x32(a[c * 64], b[c * 64], acc);
-        uint64_t m[4];
+    for (int w = w0; w < w0 + wpw; ++w) {
+        f32x4 lo = f32x4{0.f, 0.f, 0.f, 0.f}, hi = f32x4{0.f, 0.f, 0.f, 0.f};
+        const u32x4* b0 = hp_tiled + (int64_t)(2 * w) * kc * 64 + lane;
+        const u32x4* b1 = b0 + (int64_t)kc * 64;
+        for (int c = 0; c < kc; c += 4) {  // kc is a multiple of 4: twelve loads in flight per step
+            u32x4 x[4], y0[4], y1[4];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) m[j] = __ballot(acc[j] >= 0.0f);
-        // lane l < 16 owns row 4 (l / 4) + l % 4 = l of the group: its bits sit in m[l % 4] at 16 (l / 4)
-        const uint64_t mine = (lane & 3) == 0 ? m[0] : (lane & 3) == 1 ? m[1] : (lane & 3) == 2 ? m[2] : m[3];
-        const uint32_t b16 = (uint32_t)(mine >> (16 * ((lane >> 2) & 3))) & 0xFFFFu;
-        word |= b16 << (16 * (hg & 1));
-        if (hg & 1) {
-            const int64_t row = g * 16 + lane;
-            if (lane < 16 && row >= row0 && row < row0 + n) sig[row * words + (hg >> 1)] = word;
-            word = 0u;
+            for (int u = 0; u < 4; ++u) {
+                x[u] = a[(c + u) * 64];
+                y0[u] = b0[(c + u) * 64];
+                y1[u] = b1[(c + u) * 64];
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                lo = mfma16x16x32(x[u], y0[u], lo);
+                hi = mfma16x16x32(x[u], y1[u], hi);
+            }
         }
+        uint32_t word = 0u;
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+            const f32x4 acc = half ? hi : lo;
+            uint64_t m[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) m[j] = __ballot(acc[j] >= 0.0f);
+            // lane l < 16 owns row 4 (l / 4) + l % 4 = l of the group: its bits sit in m[l % 4] at 16 (l / 4)
+            const uint64_t mine = (lane & 3) == 0 ? m[0] : (lane & 3) == 1 ? m[1] : (lane & 3) == 2 ? m[2] : m[3];
+            word |= ((uint32_t)(mine >> (16 * ((lane >> 2) & 3))) & 0xFFFFu) << (16 * half);
+        }
+        const int64_t row = g * 16 + lane;
+        if (lane < 16 && row >= row0 && row < row0 + n) sig[row * words + w] = word;
     }
 }
 
@@ -66,8 +84,9 @@ __global__ __launch_bounds__(256) void k_lsh_clear(uint32_t* __restrict__ cnt, i
 }
 
 // Candidates of queries q0 .. q0+nq-1: every entry whose signature differs from the query's in at most `radius`
-// bits is appended to the query's list (at most max_cand kept; cnt counts them all).  One thread per entry,
-// the query signatures in LDS.
+// bits is appended to the query's list (at most max_cand kept; cnt counts them all).  Each thread takes
+// kScanKeys entries at a time (the query signatures, in LDS, are read once for all of them).
+constexpr int kScanKeys = 4;
 __global__ __launch_bounds__(256) void k_lsh_scan(const uint32_t* __restrict__ sig_keys, int64_t n_rows,
                                                   const uint32_t* __restrict__ sig_q, int q0, int nq, int words,
                                                   int radius, int max_cand, uint32_t* __restrict__ cnt,
@@ -75,18 +94,41 @@ __global__ __launch_bounds__(256) void k_lsh_scan(const uint32_t* __restrict__ s
     __shared__ uint32_t sq[kScanQueries * 8];
     for (int i = threadIdx.x; i < nq * words; i += 256) sq[i] = sig_q[(int64_t)q0 * words + i];
     __syncthreads();
-    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n_rows; i += (int64_t)gridDim.x * 256) {
-        uint32_t k[8];
+    const int64_t stride = (int64_t)gridDim.x * 256;
+    for (int64_t i0 = (int64_t)blockIdx.x * 256 + threadIdx.x; i0 < n_rows; i0 += kScanKeys * stride) {
+        uint32_t k[kScanKeys][8];
 #pragma unroll
-        for (int w = 0; w < 8; ++w) k[w] = w < words ? sig_keys[i * words + w] : 0u;
+        for (int e = 0; e < kScanKeys; ++e) {
+            const int64_t i = i0 + e * stride;
+            if ((words & 3) == 0) {  // 16-byte loads (signature rows are 16-byte aligned then)
+                const uint4* p = (const uint4*)(sig_keys + i * words);
+#pragma unroll
+                for (int v = 0; v < 2; ++v) {
+                    const uint4 x = (v * 4 < words && i < n_rows) ? p[v] : uint4{0u, 0u, 0u, 0u};
+                    k[e][4 * v] = x.x, k[e][4 * v + 1] = x.y, k[e][4 * v + 2] = x.z, k[e][4 * v + 3] = x.w;
+                }
+            } else {
+#pragma unroll
+                for (int w = 0; w < 8; ++w) k[e][w] = (w < words && i < n_rows) ? sig_keys[i * words + w] : 0u;
+            }
+        }
         for (int b = 0; b < nq; ++b) {
-            int h = 0;
+            int h[kScanKeys] = {};
 #pragma unroll
-            for (int w = 0; w < 8; ++w)
-                if (w < words) h += __popc(k[w] ^ sq[b * words + w]);
-            if (h <= radius) {
-                const uint32_t pos = atomicAdd(&cnt[q0 + b], 1u);
-                if (pos < (uint32_t)max_cand) cand[(int64_t)(q0 + b) * max_cand + pos] = (int32_t)i;
+            for (int w = 0; w < 8; ++w) {
+                if (w < words) {
+                    const uint32_t qw = sq[b * words + w];
+#pragma unroll
+                    for (int e = 0; e < kScanKeys; ++e) h[e] += __popc(k[e][w] ^ qw);
+                }
+            }
+#pragma unroll
+            for (int e = 0; e < kScanKeys; ++e) {
+                const int64_t i = i0 + e * stride;
+                if (i < n_rows && h[e] <= radius) {
+                    const uint32_t pos = atomicAdd(&cnt[q0 + b], 1u);
+                    if (pos < (uint32_t)max_cand) cand[(int64_t)(q0 + b) * max_cand + pos] = (int32_t)i;
+                }
             }
         }
     }
@@ -135,8 +177,13 @@ hipError_t launch_simhash(const uint16_t* rows_tiled, int d_pad, int64_t row0, i
                           int bits, uint32_t* sig, hipStream_t s) {
     if (n <= 0) return hipSuccess;
     const int64_t g0 = row0 >> 4, g1 = (row0 + n + 15) >> 4;
-    k_simhash<<<dim3((unsigned)((g1 - g0 + 3) / 4)), dim3(256), 0, s>>>(
-        (const u32x4*)rows_tiled, d_pad >> 5, row0, n, (const u32x4*)hp_tiled, bits, sig);
+    const int words = bits >> 5;
+    // few rows (a query batch): one wave per signature word, so the words of a group are computed in parallel;
+    // many rows (building the index): one wave per group, reading its rows once for every word
+    const int wpw = (g1 - g0) * words <= 4096 ? 1 : words;
+    const int64_t waves = (g1 - g0) * (words / wpw);
+    k_simhash<<<dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, s>>>(
+        (const u32x4*)rows_tiled, d_pad >> 5, row0, n, (const u32x4*)hp_tiled, bits, wpw, sig);
     return hipGetLastError();
 }
 
