@@ -10,8 +10,7 @@
 // the entries within a Hamming radius of its signature (radius 0 is equality
 // of hash keys), found by one pass over the signatures (bits / 8 bytes per
 // entry instead of the key's d * 2), and re-ranked by their exact similarity.
-#include "common.hpp"
-#include "launch.hpp"
+#include "verify.hpp"
 
 namespace lacache {
 
@@ -78,9 +77,56 @@ __global__ __launch_bounds__(256) void k_simhash(const u32x4* __restrict__ rows_
     }
 }
 
-__global__ __launch_bounds__(256) void k_lsh_clear(uint32_t* __restrict__ cnt, int B) {
-    const int i = blockIdx.x * 256 + threadIdx.x;
-    if (i < B) cnt[i] = 0u;
+// Query preparation for the LSH lookup, one workgroup of 16 waves per 16 queries: wave w normalises and
+// rounds query 16 g + w into the tiled scratch exactly as stored vectors are (zeros past the batch) and
+// clears its candidate count; after the barrier wave w < bits / 32 computes signature word w of the 16
+// queries as k_simhash does.
+__global__ __launch_bounds__(1024) void k_lsh_prep(const void* __restrict__ queries, int dtype, int nb, int d,
+                                                   int d_pad, uint16_t* __restrict__ qt,
+                                                   const u32x4* __restrict__ hp_tiled, int bits,
+                                                   uint32_t* __restrict__ sigq, uint32_t* __restrict__ cnt) {
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int g = blockIdx.x;
+    const int r = g * 16 + wv;
+    const bool live = r < nb;
+    const int kc = d_pad >> 5;
+    const char* src = (const char*)queries + (live ? (int64_t)r * d * (dtype == 0 ? 4 : 2) : 0);
+    normalise_row(src, dtype, d, d_pad, live, lane,
+                  [&](int j0, u32x4 w) { *(u32x4*)(qt + tiled_offset(r, j0, kc)) = w; });
+    if (live && lane == 0) cnt[r] = 0u;
+    __syncthreads();
+    const int words = bits >> 5;
+    if (wv >= words) return;
+    const u32x4* a = (const u32x4*)qt + (int64_t)g * kc * 64 + lane;
+    const u32x4* b0 = hp_tiled + (int64_t)(2 * wv) * kc * 64 + lane;
+    const u32x4* b1 = b0 + (int64_t)kc * 64;
+    f32x4 lo = f32x4{0.f, 0.f, 0.f, 0.f}, hi = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int c = 0; c < kc; c += 4) {
+        u32x4 x[4], y0[4], y1[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            x[u] = a[(c + u) * 64];
+            y0[u] = b0[(c + u) * 64];
+            y1[u] = b1[(c + u) * 64];
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            lo = mfma16x16x32(x[u], y0[u], lo);
+            hi = mfma16x16x32(x[u], y1[u], hi);
+        }
+    }
+    uint32_t word = 0u;
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+        const f32x4 acc = half ? hi : lo;
+        uint64_t m[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) m[j] = __ballot(acc[j] >= 0.0f);
+        const uint64_t mine = (lane & 3) == 0 ? m[0] : (lane & 3) == 1 ? m[1] : (lane & 3) == 2 ? m[2] : m[3];
+        word |= ((uint32_t)(mine >> (16 * ((lane >> 2) & 3))) & 0xFFFFu) << (16 * half);
+    }
+    const int row = g * 16 + lane;
+    if (lane < 16 && row < nb) sigq[(int64_t)row * words + wv] = word;
 }
 
 // Candidates of queries q0 .. q0+nq-1: every entry whose signature differs from the query's in at most `radius`
@@ -136,12 +182,17 @@ __global__ __launch_bounds__(256) void k_lsh_scan(const uint32_t* __restrict__ s
 
 // One wave per query: the exact similarity of each candidate (the query and the entry read from their tiled
 // stores, bf16 products summed in float32), the best as a packed top-1 (order-free: highest score, lowest
-// index), written as the query's single stage-1 partial; n_cand receives the candidate count.
-__global__ __launch_bounds__(256) void k_lsh_rerank(const u32x4* __restrict__ keys_tiled,
+// index), then the threshold and stage 2 (verify_query); n_cand receives the candidate count.
+__global__ __launch_bounds__(256) void k_lsh_verify(const u32x4* __restrict__ keys_tiled,
                                                     const u32x4* __restrict__ qt, int kc, int B,
                                                     const uint32_t* __restrict__ cnt,
                                                     const int32_t* __restrict__ cand, int max_cand,
-                                                    uint64_t* __restrict__ part, int32_t* __restrict__ n_cand) {
+                                                    int32_t* __restrict__ n_cand, int n_rows, int dtype,
+                                                    const PrefixModels M, const int32_t* __restrict__ la_tok,
+                                                    int k, const int32_t* __restrict__ tokens, int k_cap,
+                                                    float tau_q, int32_t* __restrict__ idx_out,
+                                                    float* __restrict__ score_out, float* __restrict__ resp_out,
+                                                    int32_t* __restrict__ dec_out) {
     const int lane = threadIdx.x & 63;
     const int b = blockIdx.x * 4 + (threadIdx.x >> 6);
     if (b >= B) return;
@@ -160,10 +211,9 @@ __global__ __launch_bounds__(256) void k_lsh_rerank(const u32x4* __restrict__ ke
         acc = wave_sum_f32(acc);
         best = umax64(best, pack_top1(acc, i));
     }
-    if (lane == 0) {
-        part[b] = best;
-        n_cand[b] = (int32_t)c_all;
-    }
+    if (lane == 0) n_cand[b] = (int32_t)c_all;
+    verify_query(b, best, unpack_idx(best), unpack_score(best), n_rows, dtype, M, la_tok, k, tokens, k_cap, tau_q,
+                 idx_out, score_out, resp_out, dec_out, lane);
 }
 
 hipError_t launch_tile_rows(const uint16_t* src, int rows, int d, int d_pad, uint16_t* dst, hipStream_t s) {
@@ -187,24 +237,28 @@ hipError_t launch_simhash(const uint16_t* rows_tiled, int d_pad, int64_t row0, i
     return hipGetLastError();
 }
 
-hipError_t launch_lsh_stage1(const uint16_t* keys_tiled, const uint32_t* sig_keys, int64_t n_rows,
-                             const uint16_t* qt, const uint32_t* sig_q, int B, int d_pad, int bits, int radius,
-                             int max_cand, uint32_t* cnt, int32_t* cand, uint64_t* part, int32_t* n_cand,
-                             int num_cu, hipStream_t s) {
-    if (B <= 0) return hipSuccess;
+hipError_t launch_lsh_lookup(const void* queries, int dtype, int nb, int d, int d_pad, uint16_t* qt,
+                             const uint16_t* hp_tiled, int bits, uint32_t* sigq, const uint16_t* keys_tiled,
+                             const uint32_t* sig_keys, int64_t n_rows, int radius, int max_cand, uint32_t* cnt,
+                             int32_t* cand, int32_t* n_cand, const PrefixModels& models, const int32_t* la_tok,
+                             int k, const int32_t* tokens, int k_cap, float tau_q, int32_t* idx, float* score,
+                             float* resp_score, int32_t* decision, int num_cu, hipStream_t s) {
+    if (nb <= 0) return hipSuccess;
     const int words = bits >> 5;
     if (words < 1 || words > 8) return hipErrorInvalidValue;
-    k_lsh_clear<<<dim3((unsigned)((B + 255) / 256)), dim3(256), 0, s>>>(cnt, B);
+    k_lsh_prep<<<dim3((unsigned)((nb + 15) / 16)), dim3(1024), 0, s>>>(queries, dtype, nb, d, d_pad, qt,
+                                                                      (const u32x4*)hp_tiled, bits, sigq, cnt);
     int64_t blocks = (n_rows + 255) / 256;
     if (blocks > 8 * num_cu) blocks = 8 * num_cu;
     if (blocks < 1) blocks = 1;
-    for (int q0 = 0; q0 < B && n_rows > 0; q0 += kScanQueries) {
-        const int nq = B - q0 < kScanQueries ? B - q0 : kScanQueries;
-        k_lsh_scan<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(sig_keys, n_rows, sig_q, q0, nq, words, radius,
+    for (int q0 = 0; q0 < nb && n_rows > 0; q0 += kScanQueries) {
+        const int nq = nb - q0 < kScanQueries ? nb - q0 : kScanQueries;
+        k_lsh_scan<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(sig_keys, n_rows, sigq, q0, nq, words, radius,
                                                                max_cand, cnt, cand);
     }
-    k_lsh_rerank<<<dim3((unsigned)((B + 3) / 4)), dim3(256), 0, s>>>(
-        (const u32x4*)keys_tiled, (const u32x4*)qt, d_pad >> 5, B, cnt, cand, max_cand, part, n_cand);
+    k_lsh_verify<<<dim3((unsigned)((nb + 3) / 4)), dim3(256), 0, s>>>(
+        (const u32x4*)keys_tiled, (const u32x4*)qt, d_pad >> 5, nb, cnt, cand, max_cand, n_cand, (int)n_rows,
+        dtype, models, la_tok, k, tokens, k_cap, tau_q, idx, score, resp_score, decision);
     return hipGetLastError();
 }
 

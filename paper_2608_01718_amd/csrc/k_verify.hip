@@ -1,47 +1,11 @@
 // k_verify.hip -- end of stage 1 (merge, threshold) and stage 2 (gather and verify), one wave per query.
 //
-// Stage 1 ends with the best entry over all partial candidates; it is a hit
-// when the clamped similarity is >= tau_q (Section 5.1, cache check).  Only
-// then does stage 2 run (Algorithm 1: the lookahead check sits inside the
-// hit branch): the matched entry's stored prefix -- its embedding row and its
-// first k token IDs (Section 4.2, cache structure <h(x), [h(f_k(x)), f(x)]>)
-// -- is gathered and compared with the query's lookahead.  The check passes
-// on identical tokens, or on a prefix-embedding cosine >= tau_r (Section 5.1,
-// lookahead check) -- under every one of the m prefix models when the cache
-// holds an ensemble of lookahead checks (Section 4.4).  Decisions: 0 MISS,
-// 1 REJECT, 2 HIT, 3 HIT_EXACT.
-#include "common.hpp"
-#include "launch.hpp"
+// Stage 1 ends with the best entry over all partial candidates (for the GEMM
+// path, whose partials name 32-row groups, the exact row is recovered by
+// replaying the group); the threshold and stage 2 follow in verify_query.
+#include "verify.hpp"
 
 namespace lacache {
-
-// Exact row of query b inside the 32-row group g that the GEMM path reported: replay the group against
-// the same 32-query fragment with the same MFMA sequence (v_mfma_f32_32x32x16_bf16 over the 16-column
-// steps in order, from a zero accumulator), which reproduces the GEMM's float32 scores bit for bit, and
-// take the lowest stored row whose score equals s.  Returns -1 if none does.
-__device__ int32_t replay_group(const u32x4* __restrict__ keys, const u32x4* __restrict__ qt, int kc, int b, int g,
-                                float s, int n_rows, int lane) {
-    const int kr = g * 32 + (lane & 31);       // key row this lane feeds (row operand)
-    const int qr = (b & ~31) + (lane & 31);    // query row of the fragment (column operand)
-    const u32x4* kp = keys + (int64_t)(kr >> 4) * kc * 64 + (kr & 15);
-    const u32x4* qp = qt + (int64_t)(qr >> 4) * kc * 64 + (qr & 15);
-    f32x16 acc = f32x16{};
-    for (int st = 0; st < 2 * kc; ++st) {
-        const int off = (st >> 1) * 64 + (((st & 1) << 1) + (lane >> 5)) * 16;
-        acc = mfma32x32x16(kp[off], qp[off], st == 0 ? f32x16{} : acc);
-    }
-    int row = 0x7FFFFFFF;
-    if ((lane & 31) == (b & 31)) {
-#pragma unroll
-        for (int j = 15; j >= 0; --j) {
-            const int r = g * 32 + 8 * (j >> 2) + 4 * (lane >> 5) + (j & 3);
-            if (acc[j] == s && r < n_rows) row = r;
-        }
-    }
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) row = min(row, __shfl_xor(row, m, kWave));
-    return row == 0x7FFFFFFF ? -1 : row;
-}
 
 __global__ __launch_bounds__(256) void k_finalize_verify(
     const uint64_t* __restrict__ part, int P, int part_groups, const u32x4* __restrict__ keys_tiled,
@@ -52,66 +16,16 @@ __global__ __launch_bounds__(256) void k_finalize_verify(
     const int lane = threadIdx.x & 63;
     const int b = blockIdx.x * 4 + (threadIdx.x >> 6);
     if (b >= B) return;
-    const float qnan = __uint_as_float(0x7FC00000u);
-    if (n_rows <= 0) {
-        if (lane == 0) {
-            idx_out[b] = -1;
-            score_out[b] = qnan;
-            dec_out[b] = 0;
-        }
-        if (lane < M.m) resp_out[(int64_t)b * M.m + lane] = qnan;
-        return;
-    }
     uint64_t m = 0;
-    for (int p = lane; p < P; p += kWave) m = umax64(m, part[(int64_t)b * P + p]);
-    m = wave_max_u64(m);
+    if (n_rows > 0) {
+        for (int p = lane; p < P; p += kWave) m = umax64(m, part[(int64_t)b * P + p]);
+        m = wave_max_u64(m);
+    }
     int32_t i = unpack_idx(m);
     const float s_raw = unpack_score(m);
     if (part_groups && m != 0ull) i = replay_group(keys_tiled, qt, kc, b, i, s_raw, n_rows, lane);
-    const float score = fminf(fmaxf(s_raw, -1.0f), 1.0f);
-    // every stored row yields a candidate, so m != 0 here; the range check keeps the gathers in bounds regardless
-    if (m == 0ull || i < 0 || i >= n_rows || !(score >= tau_q)) {
-        if (lane == 0) {
-            idx_out[b] = (m == 0ull) ? -1 : i;
-            score_out[b] = (m == 0ull) ? qnan : score;
-            dec_out[b] = 0;
-        }
-        if (lane < M.m) resp_out[(int64_t)b * M.m + lane] = qnan;
-        return;
-    }
-
-    // for every prefix model: normalise the lookahead embedding exactly as stored vectors are and dot it with
-    // the entry's stored prefix row; the embedding check passes only if every model reaches its threshold
-    // (Section 4.4: with m lookahead checks a hit needs all of them)
-    const size_t esz = dtype == 0 ? 4 : 2;
-    bool all_pass = true;
-    for (int mi = 0; mi < M.m; ++mi) {
-        const char* src = (const char*)M.la[mi] + (int64_t)b * M.d[mi] * esz;
-        const u32x4* er = (const u32x4*)(M.emb[mi] + (int64_t)i * M.d_pad[mi]);
-        float acc = 0.0f;
-        // padded columns are zero on both sides
-        normalise_row(src, dtype, M.d[mi], M.d_pad[mi], true, lane,
-                      [&](int j0, u32x4 w) { acc = dot8_bf16(w, er[j0 >> 3], acc); });
-        acc = wave_sum_f32(acc);
-        const float r = fminf(fmaxf(acc, -1.0f), 1.0f);
-        if (lane == 0) resp_out[(int64_t)b * M.m + mi] = r;
-        all_pass = all_pass && (r >= M.tau[mi]);
-    }
-
-    // first k tokens: lane j compares token j, 64 at a time
-    bool tok_eq = true;
-    const int32_t* ut = la_tok + (int64_t)b * k;
-    const int32_t* tt = tokens + (int64_t)i * k_cap;
-    for (int j0 = 0; j0 < k; j0 += kWave) {
-        const int j = j0 + lane;
-        const bool differ = (j < k) && (ut[j] != tt[j]);
-        if (__ballot(differ) != 0ull) tok_eq = false;
-    }
-    if (lane == 0) {
-        idx_out[b] = i;
-        score_out[b] = score;
-        dec_out[b] = tok_eq ? 3 : (all_pass ? 2 : 1);
-    }
+    verify_query(b, m, i, s_raw, n_rows, dtype, M, la_tok, k, tokens, k_cap, tau_q, idx_out, score_out, resp_out,
+                 dec_out, lane);
 }
 
 hipError_t launch_finalize_verify(const uint64_t* part, int P, bool part_groups, const uint16_t* keys_tiled,

@@ -408,12 +408,6 @@ int lacache_lookup_lsh(lacache_t h, const void* queries, const void* lookahead_e
     for (int b0 = 0; b0 < B; b0 += h->max_batch) {
         const int nb = (B - b0) < h->max_batch ? (B - b0) : h->max_batch;
         const char* q = (const char*)queries + (size_t)b0 * h->d * esz;
-        if (launch_normalise(q, h->dtype, nb, round_up(nb, 16), h->d, h->d_pad, h->qt, 0, true, s) != hipSuccess ||
-            launch_simhash(h->qt, h->d_pad, 0, nb, h->hp, h->lsh_bits, h->sigq, s) != hipSuccess ||
-            launch_lsh_stage1(h->keys, h->sig, h->size, h->qt, h->sigq, nb, h->d_pad, h->lsh_bits, radius,
-                              h->lsh_max_cand, h->lsh_cnt, h->lsh_cand, h->part, n_cand + b0, h->num_cu,
-                              s) != hipSuccess)
-            return LACACHE_EHIP;
         PrefixModels models{};
         models.m = 1;
         models.la[0] = (const char*)lookahead_emb + (size_t)b0 * h->d_resp[0] * esz;
@@ -421,9 +415,10 @@ int lacache_lookup_lsh(lacache_t h, const void* queries, const void* lookahead_e
         models.d[0] = h->d_resp[0];
         models.d_pad[0] = h->d_pad_resp[0];
         models.tau[0] = tau_r;
-        if (launch_finalize_verify(h->part, 1, false, h->keys, h->qt, nb, (int)h->size, h->dtype, h->d, models,
-                                   lookahead_tokens + (size_t)b0 * k, k, h->tokens, h->k_cap, tau_q, idx + b0,
-                                   score + b0, resp_score + b0, decision + b0, s) != hipSuccess)
+        if (launch_lsh_lookup(q, h->dtype, nb, h->d, h->d_pad, h->qt, h->hp, h->lsh_bits, h->sigq, h->keys, h->sig,
+                              h->size, radius, h->lsh_max_cand, h->lsh_cnt, h->lsh_cand, n_cand + b0, models,
+                              lookahead_tokens + (size_t)b0 * k, k, h->tokens, h->k_cap, tau_q, idx + b0,
+                              score + b0, resp_score + b0, decision + b0, h->num_cu, s) != hipSuccess)
             return LACACHE_EHIP;
     }
     return LACACHE_OK;

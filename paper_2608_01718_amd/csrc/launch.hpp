@@ -63,14 +63,17 @@ hipError_t launch_accept_length(const void* logits, int dtype, int V, const int3
 
 // LSH index (random hyperplanes): tiled copy of the raw hyperplanes, signatures of rows row0 .. row0+n-1 of a
 // tiled matrix ([rows][bits / 32] words, bit i of a row is 1 when its projection on hyperplane i is >= 0),
-// and the stage-1 search (Hamming-radius candidates, exact re-rank) writing one packed partial per query.
+// and the whole LSH lookup of a query batch (query preparation, Hamming-radius candidate scan, exact re-rank,
+// threshold and stage 2).
 hipError_t launch_tile_rows(const uint16_t* src, int rows, int d, int d_pad, uint16_t* dst, hipStream_t s);
 hipError_t launch_simhash(const uint16_t* rows_tiled, int d_pad, int64_t row0, int64_t n, const uint16_t* hp_tiled,
                           int bits, uint32_t* sig, hipStream_t s);
-hipError_t launch_lsh_stage1(const uint16_t* keys_tiled, const uint32_t* sig_keys, int64_t n_rows,
-                             const uint16_t* qt, const uint32_t* sig_q, int B, int d_pad, int bits, int radius,
-                             int max_cand, uint32_t* cnt, int32_t* cand, uint64_t* part, int32_t* n_cand,
-                             int num_cu, hipStream_t s);
+hipError_t launch_lsh_lookup(const void* queries, int dtype, int nb, int d, int d_pad, uint16_t* qt,
+                             const uint16_t* hp_tiled, int bits, uint32_t* sigq, const uint16_t* keys_tiled,
+                             const uint32_t* sig_keys, int64_t n_rows, int radius, int max_cand, uint32_t* cnt,
+                             int32_t* cand, int32_t* n_cand, const PrefixModels& models, const int32_t* la_tok,
+                             int k, const int32_t* tokens, int k_cap, float tau_q, int32_t* idx, float* score,
+                             float* resp_score, int32_t* decision, int num_cu, hipStream_t s);
 
 // Most partials a stage-1 launch may write per query.
 constexpr int kMaxPartials = 1024;
