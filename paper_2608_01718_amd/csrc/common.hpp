@@ -36,8 +36,14 @@ __host__ __device__ inline int64_t tiled_offset(int64_t row, int32_t col, int32_
 // bfloat16 grid is uniform with spacing 2^-133 (subnormals): round v*2^133 to
 // an integer.  Overflow gives infinity.
 // ---------------------------------------------------------------------------
-__device__ inline uint16_t bf16_rne_from_f64(double v) {
-    const uint64_t b = (uint64_t)__double_as_longlong(v);
+__host__ __device__ inline uint64_t f64_bits(double v) {
+    uint64_t b;
+    __builtin_memcpy(&b, &v, sizeof b);
+    return b;
+}
+
+__host__ __device__ inline uint16_t bf16_rne_from_f64(double v) {
+    const uint64_t b = f64_bits(v);
     const uint16_t sign = (uint16_t)((b >> 48) & 0x8000u);
     const uint64_t mag = b & 0x7FFFFFFFFFFFFFFFull;
     const int e = (int)(mag >> 52) - 1023;
@@ -49,6 +55,20 @@ __device__ inline uint16_t bf16_rne_from_f64(double v) {
     }
     const double s = __builtin_rint(__builtin_ldexp(__builtin_fabs(v), 133));
     return (uint16_t)(sign | (uint16_t)s);
+}
+
+// bfloat16 rounding of the quotient v / n, identical to bf16_rne_from_f64(v / n) with the division correctly
+// rounded, from q' = v * rn where rn = 1 / n correctly rounded.  q' is within 3 units in the last place of the
+// rounded quotient q, so q' and q round to the same bfloat16 unless q' lies within a few units of a rounding
+// midpoint (the 45 bits below the kept ones within 16 of 2^44) or in the subnormal range of bfloat16; those
+// rare cases divide.  Across a power of two both lie far from a midpoint and round to that power.
+__host__ __device__ inline uint16_t bf16_rne_quotient(double v, double n, double rn) {
+    const double q = v * rn;
+    const uint64_t mag = f64_bits(q) & 0x7FFFFFFFFFFFFFFFull;
+    const int e = (int)(mag >> 52) - 1023;
+    const int64_t below = (int64_t)(mag & ((1ull << 45) - 1)) - (int64_t)(1ull << 44);
+    if (e < -125 || (below <= 16 && below >= -16)) return bf16_rne_from_f64(v / n);
+    return bf16_rne_from_f64(q);
 }
 
 __device__ inline float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
@@ -135,11 +155,12 @@ __device__ inline u32x4 quantise8(const void* row, int dtype, int d, int j0, dou
     uint16_t h[8];
     double v[8];
     if (live && j0 < d && n != 0.0) load8(row, dtype, d, j0, v);
+    const double rn = 1.0 / n;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
         const int j = j0 + e;
         h[e] = 0;
-        if (live && j < d && n != 0.0) h[e] = bf16_rne_from_f64(v[e] / n);
+        if (live && j < d && n != 0.0) h[e] = bf16_rne_quotient(v[e], n, rn);
     }
     u32x4 w;
     w.x = (uint32_t)h[0] | ((uint32_t)h[1] << 16);
