@@ -52,6 +52,8 @@ def parse():
     ap.add_argument("--no-calibration", action="store_true", help="skip the threshold-calibration measurement")
     ap.add_argument("--no-accept", action="store_true", help="skip the speculative-decoding acceptance measurement")
     ap.add_argument("--no-lsh", action="store_true", help="skip the LSH-indexed lookup measurement")
+    ap.add_argument("--sweep", action="store_true",
+                    help="instead of the bench line, sweep the batch size on the 1M x 768 cache (JSON per size)")
     ap.add_argument("--no-probe", action="store_true",
                     help="skip the attainable-ceiling probe (sustained MFMA rate on random bf16, HBM streaming read)")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
@@ -417,6 +419,59 @@ def run_lsh(steps, warmup, lc, torch, synth):
                 signature_bytes=float(sp.N) * bits / 8, index_build_s=t_index)
 
 
+def run_sweep(steps, warmup, lc, torch, synth):
+    """Lookup throughput over the batch size on the 1M x 768 serving cache: the exact path (the streaming
+    kernel up to 64 queries, the GEMM kernel above) and, up to 1024 queries, the LSH path (256 bits,
+    radius 64).  Prints one JSON line per batch size."""
+    from tests.gpu_util import gpu_cache, to_dev
+    sp = synth.spec("serve_large")
+    w = synth.generate(sp)
+    c = gpu_cache(lc, sp, w.keys, w.emb, w.tokens, max_batch=sp.B, insert_chunk=1 << 18)
+    c.enable_lsh(256, to_dev(synth.hyperplanes(256, sp.d, seed=sp.seed + 1000)), 256)
+    q, a = to_dev(w.queries), to_dev(w.la_emb)
+    t = to_dev(np.ascontiguousarray(w.la_tok[:, :sp.k]))
+    rows = []
+    for B in (1, 2, 4, 8, 16, 32, 64, 128, 256, 512, 1024, 2048, 4096):
+        n_calls = max(1, min(16, sp.B // B))
+        sl = [slice(i * B, (i + 1) * B) for i in range(n_calls)]
+        res = {"B": B}
+        for path in ("exact", "lsh"):
+            if path == "lsh" and B > 1024:
+                continue
+            def call(i):
+                s_ = sl[i % n_calls]
+                if path == "exact":
+                    c.lookup(q[s_], a[s_], t[s_], sp.tau_q, sp.tau_r, sp.k)
+                else:
+                    c.lookup_lsh(q[s_], a[s_], t[s_], sp.tau_q, sp.tau_r, sp.k, 64)
+            for i in range(warmup):
+                call(i)
+            torch.cuda.synchronize()
+            if path == "exact":
+                c.profile(True)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for i in range(steps):
+                call(i)
+            e1.record()
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / steps
+            res[path] = {"ms_per_call": ms, "lookups_per_s": B / (ms * 1e-3)}
+            if path == "exact":
+                k_ms, k_n = c.profile_read()
+                c.profile(False)
+                k_avg = k_ms / max(k_n, 1)
+                res[path]["stage1_ms"] = k_avg
+                if B <= 64:
+                    res[path]["stage1_gbs"] = sp.N * sp.d * 2 / (k_avg * 1e-3) / 1e9
+                else:
+                    res[path]["stage1_tflops"] = 2.0 * B * sp.N * sp.d / (k_avg * 1e-3) / 1e12
+        print(json.dumps(res), flush=True)
+        rows.append(res)
+    c.close()
+    return rows
+
+
 def cpu_baseline(sp, w, call_b):
     """The CPU oracle, as it is, on a bounded sample: a few queries against the full cache."""
     import oracle
@@ -448,6 +503,12 @@ def main():
         sys.exit(2)
     if args.calibrate_copy_mib:
         calibrate_copy(args.calibrate_copy_mib)
+        return
+    if args.sweep:
+        import torch
+        import synth
+        import paper_2608_01718_amd as lc
+        run_sweep(args.steps, args.warmup, lc, torch, synth)
         return
     probe = None if args.no_probe else attainable_ceilings()
     import torch
