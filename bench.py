@@ -420,9 +420,11 @@ def run_lsh(steps, warmup, lc, torch, synth):
 
 
 def run_sweep(steps, warmup, lc, torch, synth):
-    """Lookup throughput over the batch size on the 1M x 768 serving cache: the exact path (the streaming
-    kernel up to 64 queries, the GEMM kernel above) and, up to 1024 queries, the LSH path (256 bits,
-    radius 64).  Prints one JSON line per batch size."""
+    """Lookup throughput over the batch size on the 1M x 768 serving cache: the exact path at the default
+    crossover (the streaming kernel up to two 64-query groups, the GEMM kernel above) and, up to 1024
+    queries, the LSH path (256 bits, radius 64); then, for 160-256 queries, the exact path with the
+    streaming kernel forced (three and four query groups, `set_small_batch(256)`), the measurement behind
+    the default crossover.  Prints one JSON line per batch size and path set."""
     from tests.gpu_util import gpu_cache, to_dev
     sp = synth.spec("serve_large")
     w = synth.generate(sp)
@@ -430,42 +432,51 @@ def run_sweep(steps, warmup, lc, torch, synth):
     c.enable_lsh(256, to_dev(synth.hyperplanes(256, sp.d, seed=sp.seed + 1000)), 256)
     q, a = to_dev(w.queries), to_dev(w.la_emb)
     t = to_dev(np.ascontiguousarray(w.la_tok[:, :sp.k]))
-    rows = []
-    for B in (1, 2, 4, 8, 16, 32, 64, 128, 256, 512, 1024, 2048, 4096):
+
+    def measure(B, path):
         n_calls = max(1, min(16, sp.B // B))
         sl = [slice(i * B, (i + 1) * B) for i in range(n_calls)]
-        res = {"B": B}
-        for path in ("exact", "lsh"):
-            if path == "lsh" and B > 1024:
-                continue
-            def call(i):
-                s_ = sl[i % n_calls]
-                if path == "exact":
-                    c.lookup(q[s_], a[s_], t[s_], sp.tau_q, sp.tau_r, sp.k)
-                else:
-                    c.lookup_lsh(q[s_], a[s_], t[s_], sp.tau_q, sp.tau_r, sp.k, 64)
-            for i in range(warmup):
-                call(i)
-            torch.cuda.synchronize()
-            if path == "exact":
-                c.profile(True)
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record()
-            for i in range(steps):
-                call(i)
-            e1.record()
-            torch.cuda.synchronize()
-            ms = e0.elapsed_time(e1) / steps
-            res[path] = {"ms_per_call": ms, "lookups_per_s": B / (ms * 1e-3)}
-            if path == "exact":
-                k_ms, k_n = c.profile_read()
-                c.profile(False)
-                k_avg = k_ms / max(k_n, 1)
-                res[path]["stage1_ms"] = k_avg
-                if B <= 64:
-                    res[path]["stage1_gbs"] = sp.N * sp.d * 2 / (k_avg * 1e-3) / 1e9
-                else:
-                    res[path]["stage1_tflops"] = 2.0 * B * sp.N * sp.d / (k_avg * 1e-3) / 1e12
+        exact = path != "lsh"
+
+        def call(i):
+            s_ = sl[i % n_calls]
+            if exact:
+                c.lookup(q[s_], a[s_], t[s_], sp.tau_q, sp.tau_r, sp.k)
+            else:
+                c.lookup_lsh(q[s_], a[s_], t[s_], sp.tau_q, sp.tau_r, sp.k, 64)
+        for i in range(warmup):
+            call(i)
+        torch.cuda.synchronize()
+        if exact:
+            c.profile(True)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for i in range(steps):
+            call(i)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        r = {"ms_per_call": ms, "lookups_per_s": B / (ms * 1e-3)}
+        if exact:
+            k_ms, k_n = c.profile_read()
+            c.profile(False)
+            k_avg = k_ms / max(k_n, 1)
+            r["stage1_ms"] = k_avg
+            # both rates: which kernel ran depends on B, d and the crossover
+            r["stage1_gbs"] = sp.N * sp.d * 2 / (k_avg * 1e-3) / 1e9
+            r["stage1_tflops"] = 2.0 * B * sp.N * sp.d / (k_avg * 1e-3) / 1e12
+        return r
+
+    rows = []
+    for B in (1, 2, 4, 8, 16, 32, 64, 128, 256, 512, 1024, 2048, 4096):
+        res = {"B": B, "exact": measure(B, "exact")}
+        if B <= 1024:
+            res["lsh"] = measure(B, "lsh")
+        print(json.dumps(res), flush=True)
+        rows.append(res)
+    c.set_small_batch(256)  # the streaming kernel's largest batch at d = 768
+    for B in (160, 192, 224, 256):
+        res = {"B": B, "exact_stream_forced": measure(B, "exact")}
         print(json.dumps(res), flush=True)
         rows.append(res)
     c.close()

@@ -1,4 +1,4 @@
-// k_stage1_stream.hip -- stage 1 for small batches (B <= 64): one pass over the keys at HBM speed.
+// k_stage1_stream.hip -- stage 1 for small batches: one pass over the keys at HBM speed.
 //
 // Stage 1 of the lookup (Algorithm 1: search the cache with the query key) is
 // an exact top-1 over every stored key by the dot product of normalised
@@ -6,27 +6,44 @@
 // far below the matrix-core/HBM balance point, so the kernel is bound by
 // reading the keys once: every wave streams a contiguous run of 16-key groups
 // (d_pad*32 contiguous bytes each) with 1 KiB coalesced loads, double
-// buffered, while the queries sit in LDS for the whole launch.  Dot products
-// run on v_mfma_f32_16x16x32_bf16 with the keys as the row operand, so each
-// lane accumulates 4 keys x 1 query and keeps a running (best score, index)
-// per query in registers; rows are visited in increasing order and only a
-// strictly larger score replaces the best, so the lowest index wins ties.
+// buffered, while the queries sit in LDS for the whole launch.  Larger
+// batches run as up to four 64-query groups: the workgroups of one key range
+// sit on the same XCD and start together, so the range comes from HBM once
+// and the other readers find it in that XCD's L2 (or the infinity cache).
+// Dot products run on v_mfma_f32_16x16x32_bf16 with the keys as the row
+// operand, so each lane accumulates 4 keys x 1 query and keeps a running
+// (best score, index) per query in registers; rows are visited in increasing
+// order and only a strictly larger score replaces the best, so the lowest
+// index wins ties.
 #include "common.hpp"
 #include "launch.hpp"
 
 namespace lacache {
 
-constexpr int kStreamWaves = 16;  // waves per workgroup; one workgroup per CU
+constexpr int kStreamWaves = 16;     // waves per workgroup; one workgroup per CU
+constexpr int kStreamMaxGroups = 4;  // query groups of one launch, each reading every key range
 
 template <int QG>
 __global__ __launch_bounds__(1024) void k_stage1_stream(const u32x4* __restrict__ keys, const u32x4* __restrict__ qt,
-                                                        int kc, int groups, int n_rows, int waves_total, int B,
-                                                        uint64_t* __restrict__ part) {
+                                                        int kc, int groups, int n_rows, int n_ranges, int n_qgroups,
+                                                        int B, uint64_t* __restrict__ part) {
     extern __shared__ u32x4 smem[];
     u32x4* qs = smem;                                        // [QG][kc][64] query fragments
     uint64_t* red = (uint64_t*)(smem + QG * kc * 64);        // [kStreamWaves][QG * 16]
     const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-    for (int i = tid; i < QG * kc * 64; i += kStreamWaves * 64) qs[i] = qt[i];
+    // workgroup -> (query group h of 16 * QG queries, key range r).  Dispatch is round-robin over the 8 XCDs:
+    // with n_ranges % 8 == 0 the n_qgroups workgroups of a range are consecutive on one XCD.
+    int h, r;
+    if (n_qgroups > 1 && n_ranges % 8 == 0) {
+        const int xcd = blockIdx.x % 8, j = blockIdx.x / 8;
+        h = j % n_qgroups;
+        r = (j / n_qgroups) * 8 + xcd;
+    } else {
+        h = blockIdx.x % n_qgroups;
+        r = blockIdx.x / n_qgroups;
+    }
+    const u32x4* qg = qt + (int64_t)h * QG * kc * 64;       // 16 * QG query rows of the tiled scratch
+    for (int i = tid; i < QG * kc * 64; i += kStreamWaves * 64) qs[i] = qg[i];
     __syncthreads();
 
     float best[QG];
@@ -38,7 +55,8 @@ __global__ __launch_bounds__(1024) void k_stage1_stream(const u32x4* __restrict_
     }
 
     // contiguous, balanced split of the 16-key groups over all waves of the grid
-    const int64_t w = (int64_t)blockIdx.x * kStreamWaves + wid;
+    const int64_t waves_total = (int64_t)n_ranges * kStreamWaves;
+    const int64_t w = (int64_t)r * kStreamWaves + wid;
     const int g0 = (int)(w * groups / waves_total);
     const int g1 = (int)((w + 1) * groups / waves_total);
     const int nchunks = (g1 - g0) * kc;
@@ -95,16 +113,17 @@ __global__ __launch_bounds__(1024) void k_stage1_stream(const u32x4* __restrict_
         if (lane < 16) red[wid * (QG * 16) + q * 16 + lane] = p;
     }
     __syncthreads();
-    if (tid < QG * 16 && tid < B) {
+    const int q = h * QG * 16 + tid;  // query of the batch
+    if (tid < QG * 16 && q < B) {
         uint64_t m = 0;
         for (int v = 0; v < kStreamWaves; ++v) m = umax64(m, red[v * (QG * 16) + tid]);
-        part[(int64_t)tid * gridDim.x + blockIdx.x] = m;
+        part[(int64_t)q * n_ranges + r] = m;
     }
 }
 
 template <int QG>
-static hipError_t launch_qg(const u32x4* keys, const u32x4* qt, int kc, int groups, int n_rows, int nwg, int B,
-                            uint64_t* part, hipStream_t s) {
+static hipError_t launch_qg(const u32x4* keys, const u32x4* qt, int kc, int groups, int n_rows, int n_ranges,
+                            int n_qgroups, int B, uint64_t* part, hipStream_t s) {
     const size_t lds = (size_t)QG * kc * 1024 + (size_t)kStreamWaves * QG * 16 * 8;
     static bool attr_set = false;
     if (!attr_set) {
@@ -113,8 +132,8 @@ static hipError_t launch_qg(const u32x4* keys, const u32x4* qt, int kc, int grou
         if (e != hipSuccess) return e;
         attr_set = true;
     }
-    k_stage1_stream<QG><<<dim3(nwg), dim3(kStreamWaves * 64), lds, s>>>(keys, qt, kc, groups, n_rows,
-                                                                         nwg * kStreamWaves, B, part);
+    k_stage1_stream<QG><<<dim3(n_ranges * n_qgroups), dim3(kStreamWaves * 64), lds, s>>>(
+        keys, qt, kc, groups, n_rows, n_ranges, n_qgroups, B, part);
     return hipGetLastError();
 }
 
@@ -131,22 +150,39 @@ hipError_t launch_stage1_stream(const uint16_t* keys, const uint16_t* qt, int B,
                                 uint64_t* part, int num_cu, int* P_out, hipStream_t s) {
     const int kc = d_pad / 32;
     const int groups = (n_rows + 15) / 16;
-    const int qg = (B + 15) / 16;
-    if (qg < 1 || qg > stream_max_qg(d_pad) || kc % 4 != 0 || n_rows <= 0) return hipErrorInvalidValue;
-    // one workgroup per CU, fewer when there is too little work to give every wave >= 4 groups
-    int nwg = (groups + kStreamWaves * 4 - 1) / (kStreamWaves * 4);
-    if (nwg > num_cu) nwg = num_cu;
-    if (nwg > kMaxPartials) nwg = kMaxPartials;
-    if (nwg < 1) nwg = 1;
-    *P_out = nwg;
+    const int maxqg = stream_max_qg(d_pad);
+    if (maxqg < 1 || kc % 4 != 0 || n_rows <= 0 || B < 1) return hipErrorInvalidValue;
+    // up to 16 * maxqg queries in one group; more as up to kStreamMaxGroups full groups (query rows
+    // zero-padded to a multiple of 16 * maxqg by the caller)
+    const int grp = 16 * maxqg;
+    const int n_qgroups = (B + grp - 1) / grp;
+    if (n_qgroups > kStreamMaxGroups) return hipErrorInvalidValue;
+    const int qg = n_qgroups == 1 ? (B + 15) / 16 : maxqg;
+    // one workgroup per CU, fewer when there is too little work to give every wave >= 4 groups; with several
+    // query groups a multiple of 8 ranges keeps each range's workgroups on one XCD
+    int cap = num_cu / n_qgroups;
+    if (n_qgroups > 1 && cap >= 8) cap = cap / 8 * 8;
+    int n_ranges = (groups + kStreamWaves * 4 - 1) / (kStreamWaves * 4);
+    if (n_ranges > cap) n_ranges = cap;
+    if (n_ranges > kMaxPartials) n_ranges = kMaxPartials;
+    if (n_ranges < 1) n_ranges = 1;
+    *P_out = n_ranges;
     const u32x4* k4 = (const u32x4*)keys;
     const u32x4* q4 = (const u32x4*)qt;
     switch (qg) {
-        case 1: return launch_qg<1>(k4, q4, kc, groups, n_rows, nwg, B, part, s);
-        case 2: return launch_qg<2>(k4, q4, kc, groups, n_rows, nwg, B, part, s);
-        case 3: return launch_qg<3>(k4, q4, kc, groups, n_rows, nwg, B, part, s);
-        default: return launch_qg<4>(k4, q4, kc, groups, n_rows, nwg, B, part, s);
+        case 1: return launch_qg<1>(k4, q4, kc, groups, n_rows, n_ranges, n_qgroups, B, part, s);
+        case 2: return launch_qg<2>(k4, q4, kc, groups, n_rows, n_ranges, n_qgroups, B, part, s);
+        case 3: return launch_qg<3>(k4, q4, kc, groups, n_rows, n_ranges, n_qgroups, B, part, s);
+        default: return launch_qg<4>(k4, q4, kc, groups, n_rows, n_ranges, n_qgroups, B, part, s);
     }
 }
+
+// Largest batch the streaming kernel takes for d_pad columns.
+int stream_max_batch(int d_pad) { return kStreamMaxGroups * 16 * stream_max_qg(d_pad); }
+
+// Default crossover: two query groups.  Measured on 1M x 768 keys, two groups read the keys at ~5.5 TB/s
+// (0.28 ms against the GEMM kernel's 0.39 ms); with three or four groups each CU's share of the
+// contraction is the limit and the GEMM kernel is within 4 % or faster.
+int stream_default_batch(int d_pad) { return 2 * 16 * stream_max_qg(d_pad); }
 
 }  // namespace lacache

@@ -13,6 +13,8 @@
 
 namespace lacache {
 int stream_max_qg(int d_pad);
+int stream_max_batch(int d_pad);
+int stream_default_batch(int d_pad);
 }
 
 using namespace lacache;
@@ -21,7 +23,7 @@ struct lacache_s {
     int device = 0;
     int64_t cap = 0, cap_pad = 0, size = 0;
     int d = 0, d_pad = 0, k_cap = 0, dtype = 0, max_batch = 0, mb_pad = 0;
-    int num_cu = 0, b_small = 64;
+    int num_cu = 0, b_small = 128;
     int m = 1;                 // prefix models (lookahead checks) per entry
     int d_resp[kMaxModels] = {}, d_pad_resp[kMaxModels] = {};
     uint16_t* keys = nullptr;  // tiled [cap_pad][d_pad]
@@ -161,7 +163,7 @@ int lacache_create_ensemble(lacache_t* out, int64_t capacity, int32_t d, int32_t
         return LACACHE_EHIP;
     }
     h->num_cu = prop.multiProcessorCount;
-    if (stream_max_qg(h->d_pad) < 4) h->b_small = 16 * stream_max_qg(h->d_pad);
+    h->b_small = stream_default_batch(h->d_pad);
 
     int rc = LACACHE_OK;
     if (rc == LACACHE_OK) rc = alloc_zero((void**)&h->keys, (size_t)h->cap_pad * h->d_pad * 2);
@@ -243,7 +245,9 @@ static int lookup_chunk(lacache_t h, const char* queries, const PrefixModels& mo
     int P = 0;
     const bool small = B <= h->b_small;
     if (n_rows > 0) {
-        const int64_t rows_pad = small ? round_up(B, 16) : round_up(B, kRowTile);
+        // the streaming kernel runs more than one query group on whole groups of 16 * stream_max_qg rows
+        const int64_t grp = 16 * (int64_t)stream_max_qg(h->d_pad);
+        const int64_t rows_pad = small ? (B <= grp ? round_up(B, 16) : round_up(B, grp)) : round_up(B, kRowTile);
         if (launch_normalise(queries, h->dtype, B, rows_pad, h->d, h->d_pad, h->qt, 0, true, s) != hipSuccess)
             return LACACHE_EHIP;
         hipEvent_t e0 = nullptr, e1 = nullptr;
@@ -438,7 +442,7 @@ int lacache_export_signatures(lacache_t h, int64_t first, int32_t n, uint32_t* s
 }
 
 int lacache_set_small_batch(lacache_t h, int32_t b_small) {
-    if (!h || b_small < 0 || b_small > 16 * stream_max_qg(h->d_pad)) return LACACHE_EINVAL;
+    if (!h || b_small < 0 || b_small > stream_max_batch(h->d_pad)) return LACACHE_EINVAL;
     h->b_small = b_small;
     return LACACHE_OK;
 }

@@ -161,25 +161,31 @@ def _edge(lc, N, d, B, k_cap, k, dtype=oracle.F32, seed=0, b_small=None, neg=Fal
     return w, g, o
 
 
-@pytest.mark.parametrize("N,d,B,k_cap,k", [
-    (1, 64, 5, 1, 1),          # a single entry
-    (17, 64, 16, 8, 8),        # one live row in the last 16-row group
-    (255, 100, 17, 150, 150),  # d not a multiple of 128, k > 64 (two ballot rounds), ragged B
-    (257, 384, 63, 20, 1),     # k = 1
-    (1000, 384, 65, 64, 64),   # B just past the small-batch limit
-    (4097, 768, 300, 16, 16),  # ragged everything on the large-batch path
-    (300, 1024, 1, 32, 32),    # B = 1
+# b_small None keeps the default crossover (two streaming query groups, 128 queries for d <= 1152)
+@pytest.mark.parametrize("N,d,B,k_cap,k,b_small", [
+    (1, 64, 5, 1, 1, None),          # a single entry
+    (17, 64, 16, 8, 8, None),        # one live row in the last 16-row group
+    (255, 100, 17, 150, 150, None),  # d not a multiple of 128, k > 64 (two ballot rounds), ragged B
+    (257, 384, 63, 20, 1, None),     # k = 1
+    (1000, 384, 65, 64, 64, None),   # B just past one streaming query group: two groups of 64
+    (2000, 768, 128, 16, 16, None),  # two full streaming query groups, the default limit
+    (1000, 384, 129, 64, 64, None),  # just past the default limit: the GEMM path
+    (1500, 768, 200, 16, 16, 256),   # four streaming query groups, the last one ragged
+    (1000, 1152, 256, 64, 64, 256),  # the largest streaming batch, at the largest d it holds
+    (900, 1280, 150, 8, 8, 192),     # d > 1152: groups of 48 queries, four of them, the last holding 6
+    (4097, 768, 300, 16, 16, None),  # ragged everything on the large-batch path
+    (300, 1024, 1, 32, 32, None),    # B = 1
 ])
 @pytest.mark.parametrize("dtype", [oracle.F32, oracle.BF16])
-def test_edge_shapes(lc, N, d, B, k_cap, k, dtype):
-    _edge(lc, N, d, B, k_cap, k, dtype)
+def test_edge_shapes(lc, N, d, B, k_cap, k, b_small, dtype):
+    _edge(lc, N, d, B, k_cap, k, dtype, b_small=b_small)
 
 
-@pytest.mark.parametrize("b_small", [0, 64])
-def test_all_negative_scores_never_pick_padding(lc, b_small):
+@pytest.mark.parametrize("b_small,B", [(0, 40), (64, 40), (128, 100), (256, 200)])
+def test_all_negative_scores_never_pick_padding(lc, b_small, B):
     # every real score is negative; padded rows (zeros) would score 0 if they were not masked
     for N in (1, 17, 250):
-        _, g, o = _edge(lc, N, 64, 40, 4, 4, neg=True, b_small=b_small, seed=N)
+        _, g, o = _edge(lc, N, 64, B, 4, 4, neg=True, b_small=b_small, seed=N)
         assert np.all(g["idx"] < N) and np.all(g["score"] < 0)
 
 
@@ -201,9 +207,10 @@ def test_empty_cache(lc):
     c.close()
 
 
-def test_determinism_and_paths_agree(lc):
+@pytest.mark.parametrize("B", [64, 100, 128, 200, 256])
+def test_determinism_and_paths_agree(lc, B):
     import torch
-    sp = synth.spec("mid", N=20_000, B=64)
+    sp = synth.spec("mid", N=20_000, B=B)
     w = synth.generate(sp)
     c = gpu_cache(lc, sp, w.keys, w.emb, w.tokens)
     runs = [gpu_lookup(c, w.queries, w.la_emb, w.la_tok, sp.tau_q, sp.tau_r, sp.k) for _ in range(5)]
@@ -266,7 +273,7 @@ def test_errors_with_live_handle(lc):
     with pytest.raises(lc.LaCacheError):
         c.lookup(q, q, t[:4], 0.5, float("inf"), 4)
     with pytest.raises(lc.LaCacheError):
-        c.set_small_batch(65)
+        c.set_small_batch(257)
     with pytest.raises(ValueError):
         c.lookup(q.double(), q, t[:4], 0.5, 0.5, 4)
     # a lookup with more queries than max_batch runs in chunks and matches chunk-by-chunk lookups
