@@ -52,6 +52,8 @@ def parse():
     ap.add_argument("--no-calibration", action="store_true", help="skip the threshold-calibration measurement")
     ap.add_argument("--no-accept", action="store_true", help="skip the speculative-decoding acceptance measurement")
     ap.add_argument("--no-lsh", action="store_true", help="skip the LSH-indexed lookup measurement")
+    ap.add_argument("--no-large", action="store_true",
+                    help="skip the 4M x 1024 clustered workload with interleaved inserts")
     ap.add_argument("--sweep", action="store_true",
                     help="instead of the bench line, sweep the batch size on the 1M x 768 cache (JSON per size)")
     ap.add_argument("--no-probe", action="store_true",
@@ -419,6 +421,98 @@ def run_lsh(steps, warmup, lc, torch, synth):
                 signature_bytes=float(sp.N) * bits / 8, index_build_s=t_index)
 
 
+def run_large_interleaved(lc, torch, synth, epochs=8, per_epoch=8, batch=4096):
+    """The clustered workload (4,000,000 x 1024 bf16 keys around 10,000 centroids, k = 32, 1024 queries
+    per lookup) on its serving schedule: 8 lookups, then an insert of 4096 new clustered entries, repeated
+    8 times; from the second round on 10 % of the planted queries aim at the latest insert batch.  Every
+    lookup and insert of the schedule is in the timed region (inputs resident in HBM beforehand);
+    `value` is queries served per second over the whole cycle.  The stage-1 kernel time comes from a
+    profiled pass of 8 more lookups at the final size."""
+    from tests.gpu_util import gpu_cache, to_dev
+    sp = synth.spec("large")
+    total = sp.N + epochs * batch
+    t0 = time.time()
+    keys, emb, tok = synth.entries(sp, 0, total)
+    c = gpu_cache(lc, sp, keys[:sp.N], emb[:sp.N], tok[:sp.N], capacity=total, max_batch=sp.B,
+                  insert_chunk=1 << 18)
+    ins, pools = [], []
+    for e in range(epochs):
+        n = sp.N + e * batch
+        ins.append((to_dev(keys[n:n + batch]), to_dev(emb[n:n + batch]), to_dev(tok[n:n + batch])))
+        recent = (n - batch, n) if e > 0 else None
+        q = synth.queries(sp, keys, emb, tok, np.zeros((0, 2), np.int64), B=per_epoch * sp.B, N=n,
+                          stream_chunk=500 + e, recent=recent)
+        pools.append(dict(q=to_dev(q["queries"]), a=to_dev(q["la_emb"]),
+                          t=to_dev(np.ascontiguousarray(q["la_tok"][:, :sp.k])), cls=q["cls"], target=q["target"],
+                          recent=recent))
+    del keys, emb, tok
+    log(f"[bench] large_interleaved: store, insert batches and query pools ready in {time.time() - t0:.1f}s")
+    dev = torch.device("cuda", 0)
+    outs = [[tuple(torch.empty(sp.B, dtype=dt, device=dev) for dt in (torch.int32, torch.float32, torch.float32,
+                                                                       torch.int32)) for _ in range(per_epoch)]
+            for _ in range(epochs)]
+
+    def lookup(e, j):
+        p, s_ = pools[e], slice(j * sp.B, (j + 1) * sp.B)
+        c.lookup(p["q"][s_], p["a"][s_], p["t"][s_], sp.tau_q, sp.tau_r, sp.k, out=outs[e][j])
+
+    for j in range(2):  # warm-up at the initial size
+        lookup(0, j)
+    torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(epochs)]
+    for e in range(epochs):
+        ev[e][0].record()
+        for j in range(per_epoch):
+            lookup(e, j)
+        ev[e][1].record()
+        first = c.insert(*ins[e])
+        assert first == sp.N + e * batch
+        ev[e][2].record()
+    torch.cuda.synchronize()
+    total_ms = ev[0][0].elapsed_time(ev[-1][2])
+    lookup_ms = sum(ev[e][0].elapsed_time(ev[e][1]) for e in range(epochs))
+    insert_ms = sum(ev[e][1].elapsed_time(ev[e][2]) for e in range(epochs))
+    n_lookups = epochs * per_epoch
+
+    dec = np.concatenate([np.concatenate([outs[e][j][3].cpu().numpy() for j in range(per_epoch)])
+                          for e in range(epochs)])
+    idx = np.concatenate([np.concatenate([outs[e][j][0].cpu().numpy() for j in range(per_epoch)])
+                          for e in range(epochs)])
+    cls = np.concatenate([p["cls"] for p in pools])
+    target = np.concatenate([p["target"] for p in pools])
+    aimed = np.concatenate([(p["target"] >= p["recent"][0]) if p["recent"] else np.zeros(len(p["cls"]), bool)
+                            for p in pools]) & (cls == synth.CLS_BENIGN)
+    served = np.isin(dec, [2, 3])
+    rates = dict(benign_hit_rate=float(served[cls == synth.CLS_BENIGN].mean()),
+                 attack_hit_rate=float(served[cls == synth.CLS_COLLISION].mean()),
+                 miss_rate_of_misses=float((dec[cls == synth.CLS_MISS] == 0).mean()),
+                 latest_batch_found=float(np.mean(served[aimed] & (idx[aimed] == target[aimed]))),
+                 latest_batch_queries=int(aimed.sum()))
+
+    c.profile(True)
+    for j in range(per_epoch):
+        lookup(epochs - 1, j)
+    torch.cuda.synchronize()
+    k_ms, k_n = c.profile_read()
+    c.profile(False)
+    k_avg = k_ms / max(k_n, 1)
+    n_final = sp.N + epochs * batch
+    achieved = 2.0 * sp.B * n_final * sp.d / (k_avg * 1e-3) / 1e12
+    c.close()
+    del pools, ins, outs
+    torch.cuda.empty_cache()
+    return dict(workload=(f"large: N={sp.N:,} clustered entries (10,000 centroids) growing by {batch} per insert to "
+                          f"{n_final:,}, d={sp.d} bf16, k={sp.k}, B={sp.B} queries per lookup, {per_epoch} lookups "
+                          f"then one insert, {epochs} times"),
+                value=n_lookups * sp.B / (total_ms * 1e-3), unit="lookups/s",
+                ms_per_lookup=lookup_ms / n_lookups, ms_per_insert=insert_ms / epochs,
+                insert_entries_per_s=epochs * batch / (insert_ms * 1e-3),
+                stage1_kernel_avg_ms=k_avg,
+                roofline=dict(bound="mfma", achieved=achieved, peak=PEAK_BF16_TFLOPS, unit="TFLOP/s",
+                              frac=achieved / PEAK_BF16_TFLOPS),
+                rates=rates)
+
+
 def run_sweep(steps, warmup, lc, torch, synth):
     """Lookup throughput over the batch size on the 1M x 768 serving cache: the exact path at the default
     crossover (the streaming kernel up to two 64-query groups, the GEMM kernel above) and, up to 1024
@@ -540,6 +634,7 @@ def main():
     calibration = None if args.no_calibration else run_calibration(args.steps, args.warmup, lc, torch, synth)
     accept = None if args.no_accept else run_accept(args.steps, args.warmup, lc, torch, synth)
     lsh = None if args.no_lsh else run_lsh(args.steps, args.warmup, lc, torch, synth)
+    large = None if args.no_large else run_large_interleaved(lc, torch, synth)
 
     line = {
         "metric": "cache lookups/sec (2-stage) at N=1M,d=768; % HBM / MFMA roofline",
@@ -575,6 +670,8 @@ def main():
         line["accept"] = accept
     if lsh:
         line["lsh"] = lsh
+    if large:
+        line["large_interleaved"] = large
     if probe:
         # the same kernels rated against what this GPU sustains: MFMA throughput on random bf16 operands
         # (operand-dependent power lowers the clock below the datasheet's) and a plain streaming read
