@@ -58,17 +58,41 @@ __host__ __device__ inline uint16_t bf16_rne_from_f64(double v) {
 }
 
 // bfloat16 rounding of the quotient v / n, identical to bf16_rne_from_f64(v / n) with the division correctly
-// rounded, from q' = v * rn where rn = 1 / n correctly rounded.  q' is within 3 units in the last place of the
-// rounded quotient q, so q' and q round to the same bfloat16 unless q' lies within a few units of a rounding
-// midpoint (the 45 bits below the kept ones within 16 of 2^44) or in the subnormal range of bfloat16; those
-// rare cases divide.  Across a power of two both lie far from a midpoint and round to that power.
+// rounded, from q' = v * rn where rn = 1 / n correctly rounded.  q' is within 3 units in the last place of a
+// double of the rounded quotient q.  q' is rounded once more, to float32, and that to bfloat16.  Every
+// bfloat16 rounding midpoint is a float32, so the float32 lies on the same side of each midpoint as q' unless
+// it is that midpoint (its low 16 bits are 0x8000), and a midpoint between q' and q, 3 double units away at
+// most, would make the float32 that midpoint too.  So the result is exact unless the float32 is a midpoint;
+// those rare cases, zero and values below 2^-125 (where bfloat16 loses precision) divide.
+// The rounding without the division: the result as the float32 of the same value (its low 16 bits zero),
+// and whether it may be wrong (the float32 is a midpoint, zero, or below 2^-125), when the caller must take
+// bf16_rne_quotient_f32 instead.
+__host__ __device__ inline float bf16_rne_quotient_fast(double v, double rn, bool& exact_needed) {
+    const float f = (float)(v * rn);
+    uint32_t u;
+    __builtin_memcpy(&u, &f, 4);
+    exact_needed = (u & 0x7FFFFFFFu) < 0x01000000u || (u & 0xFFFFu) == 0x8000u;
+    u = (u + 0x7FFFu + ((u >> 16) & 1u)) & 0xFFFF0000u;
+    float r;
+    __builtin_memcpy(&r, &u, 4);
+    return r;
+}
+
+// The result as the float32 of the same value (its low 16 bits zero).
+__host__ __device__ inline float bf16_rne_quotient_f32(double v, double n, double rn) {
+    bool exact_needed;
+    const float r = bf16_rne_quotient_fast(v, rn, exact_needed);
+    if (!exact_needed) return r;
+    const uint32_t u = (uint32_t)bf16_rne_from_f64(v / n) << 16;
+    float e;
+    __builtin_memcpy(&e, &u, 4);
+    return e;
+}
 __host__ __device__ inline uint16_t bf16_rne_quotient(double v, double n, double rn) {
-    const double q = v * rn;
-    const uint64_t mag = f64_bits(q) & 0x7FFFFFFFFFFFFFFFull;
-    const int e = (int)(mag >> 52) - 1023;
-    const int64_t below = (int64_t)(mag & ((1ull << 45) - 1)) - (int64_t)(1ull << 44);
-    if (e < -125 || (below <= 16 && below >= -16)) return bf16_rne_from_f64(v / n);
-    return bf16_rne_from_f64(q);
+    const float r = bf16_rne_quotient_f32(v, n, rn);
+    uint32_t u;
+    __builtin_memcpy(&u, &r, 4);
+    return (uint16_t)(u >> 16);
 }
 
 __device__ inline float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
@@ -79,9 +103,9 @@ __device__ inline double load_in(const void* row, int dtype, int j) {
     return (double)bf16_to_f32(((const uint16_t*)row)[j]);
 }
 
-// Elements j0 .. j0+7 of a row as doubles (0 beyond d): one or two 16-byte loads when the chunk is whole
-// and 16-byte aligned, element loads otherwise.  The values are the same either way.
-__device__ inline void load8(const void* row, int dtype, int d, int j0, double v[8]) {
+// Elements j0 .. j0+7 of a row as floats (0 beyond d; bfloat16 widens exactly): one or two 16-byte loads when
+// the chunk is whole and 16-byte aligned, element loads otherwise.  The values are the same either way.
+__device__ inline void load8f(const void* row, int dtype, int d, int j0, float v[8]) {
     const size_t esz = dtype == 0 ? 4 : 2;
     const char* p = (const char*)row + (size_t)j0 * esz;
     if (j0 + 8 <= d && ((uintptr_t)p & 15) == 0) {
@@ -93,14 +117,24 @@ __device__ inline void load8(const void* row, int dtype, int d, int j0, double v
             const uint32_t w[4] = {x.x, x.y, x.z, x.w};
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
-                v[2 * t] = (double)__uint_as_float(w[t] << 16);
-                v[2 * t + 1] = (double)__uint_as_float(w[t] & 0xFFFF0000u);
+                v[2 * t] = __uint_as_float(w[t] << 16);
+                v[2 * t + 1] = __uint_as_float(w[t] & 0xFFFF0000u);
             }
         }
         return;
     }
 #pragma unroll
-    for (int e = 0; e < 8; ++e) v[e] = (j0 + e < d) ? load_in(row, dtype, j0 + e) : 0.0;
+    for (int e = 0; e < 8; ++e)
+        v[e] = (j0 + e < d) ? (dtype == 0 ? ((const float*)row)[j0 + e] : bf16_to_f32(((const uint16_t*)row)[j0 + e]))
+                            : 0.0f;
+}
+
+// The same elements as doubles.
+__device__ inline void load8(const void* row, int dtype, int d, int j0, double v[8]) {
+    float f[8];
+    load8f(row, dtype, d, j0, f);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = (double)f[e];
 }
 
 // ---------------------------------------------------------------------------

@@ -10,8 +10,8 @@
 // say; this is numpy's default), from the two order statistics floor(h) and
 // floor(h) + 1, which an exact radix select finds without sorting: three
 // histogram passes over the orderable 32-bit keys of the similarities (11,
-// 11 and 10 bits), each followed by a one-wave scan that fixes those bits of
-// both ranks' keys.
+// 11 and 10 bits), each followed by a one-workgroup scan that fixes those
+// bits of both ranks' keys.
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -26,7 +26,12 @@ __constant__ const int kBits[kPasses] = {11, 11, 10};
 
 }  // namespace
 
-// One wave per pair: normalise a[j] and b[j] as stored vectors are, and dot the rounded values.
+// One wave per pair: normalise a[j] and b[j] as stored vectors are, and dot the rounded values in column order
+// per lane, then across the wave.  The rounded values are used as float32 directly (a bfloat16 is a float32
+// with zero low bits); products of two are exact.  NC > 0: d <= 512 NC and each lane keeps its 8 NC columns of
+// both rows in registers, read once; the norms are summed in the order row_norm uses, so the rounded values
+// are those of the stored vectors.  NC = 0: any d, the rows read once for the norms and once for the dot.
+template <int NC>
 __global__ __launch_bounds__(256) void k_pair_cosine(const void* __restrict__ a, const void* __restrict__ b,
                                                      int dtype, int d, int64_t n, float* __restrict__ sims) {
     const int lane = threadIdx.x & 63;
@@ -35,11 +40,50 @@ __global__ __launch_bounds__(256) void k_pair_cosine(const void* __restrict__ a,
     const size_t esz = dtype == 0 ? 4 : 2;
     const char* ra = (const char*)a + j * d * esz;
     const char* rb = (const char*)b + j * d * esz;
-    const double na = row_norm(ra, dtype, d, true, lane);
-    const double nb = row_norm(rb, dtype, d, true, lane);
     float acc = 0.0f;
-    for (int j0 = lane * 8; j0 < d; j0 += 512)
-        acc = dot8_bf16(quantise8(ra, dtype, d, j0, na, true), quantise8(rb, dtype, d, j0, nb, true), acc);
+    if constexpr (NC > 0) {
+        float xa[NC][8], xb[NC][8];
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            load8f(ra, dtype, d, lane * 8 + 512 * c, xa[c]);
+            load8f(rb, dtype, d, lane * 8 + 512 * c, xb[c]);
+        }
+        double sa = 0.0, sb = 0.0;
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                sa += (double)xa[c][e] * (double)xa[c][e];
+                sb += (double)xb[c][e] * (double)xb[c][e];
+            }
+        const double na = __builtin_sqrt(wave_sum_f64(sa)), nb = __builtin_sqrt(wave_sum_f64(sb));
+        if (na != 0.0 && nb != 0.0) {  // a zero vector normalises to zero and scores 0
+            const double rna = 1.0 / na, rnb = 1.0 / nb;
+#pragma unroll
+            for (int c = 0; c < NC; ++c)
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    if (lane * 8 + 512 * c + e >= d) continue;
+                    acc += bf16_rne_quotient_f32(xa[c][e], na, rna) * bf16_rne_quotient_f32(xb[c][e], nb, rnb);
+                }
+        }
+    } else {
+        const double na = row_norm(ra, dtype, d, true, lane);
+        const double nb = row_norm(rb, dtype, d, true, lane);
+        if (na != 0.0 && nb != 0.0) {
+            const double rna = 1.0 / na, rnb = 1.0 / nb;
+            for (int j0 = lane * 8; j0 < d; j0 += 512) {
+                double va[8], vb[8];
+                load8(ra, dtype, d, j0, va);
+                load8(rb, dtype, d, j0, vb);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    if (j0 + e >= d) continue;
+                    acc += bf16_rne_quotient_f32(va[e], na, rna) * bf16_rne_quotient_f32(vb[e], nb, rnb);
+                }
+            }
+        }
+    }
     acc = wave_sum_f32(acc);
     if (lane == 0) sims[j] = fminf(fmaxf(acc, -1.0f), 1.0f);
 }
@@ -81,41 +125,59 @@ __global__ __launch_bounds__(256) void k_select_hist(const float* __restrict__ s
         if (h[i] != 0u) atomicAdd(&hist[i], h[i]);
 }
 
-// One wave: for each rank, the bin holding it (counts scanned in bin order) fixes this pass's bits of its
-// key; the counts of the bins before it are skipped.  The histogram is cleared for the next pass.
-__global__ __launch_bounds__(64) void k_select_scan(int pass, uint32_t* __restrict__ state,
-                                                    uint32_t* __restrict__ hist) {
-    const int lane = threadIdx.x;
-    const int shift = kShift[pass], nb = 1 << kBits[pass];
-    for (int k = 0; k < 2; ++k) {
-        const uint32_t rank = state[2 + k];
-        uint32_t before = 0u;  // count of the bins already passed
-        int bin = -1;
-        uint32_t skip = 0u;
-        for (int c = 0; c < nb && bin < 0; c += 64) {
-            const uint32_t v = hist[k * kBins + c + lane];
-            uint32_t incl = v;
+// One workgroup: for each rank, the bin holding it (counts scanned in bin order) fixes this pass's bits of its
+// key; the counts of the bins before it are skipped.  Each thread takes nb / 256 consecutive bins, a block-wide
+// exclusive scan gives the count before them, and the one thread whose bins hold the rank walks them.  The
+// histogram is cleared for the next pass.
+__global__ __launch_bounds__(256) void k_select_scan(int pass, uint32_t* __restrict__ state,
+                                                     uint32_t* __restrict__ hist) {
+    constexpr int kPer = kBins / 256;  // bins per thread in the widest pass
+    __shared__ uint32_t wsum[2][4];
+    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+    const int shift = kShift[pass], per = (1 << kBits[pass]) / 256;
+    const uint32_t rank[2] = {state[2], state[3]};
+    uint32_t cnt[2][kPer], tot[2] = {0u, 0u};
 #pragma unroll
-            for (int o = 1; o < 64; o <<= 1) {
-                const uint32_t t = __shfl_up(incl, o, kWave);
-                if (lane >= o) incl += t;
-            }
-            const uint32_t excl = incl - v;
-            const bool here = before + excl <= rank && rank < before + incl;
-            const uint64_t hit = __ballot(here);
-            if (hit != 0ull) {
-                const int l = __ffsll((unsigned long long)hit) - 1;
-                bin = c + l;
-                skip = before + __shfl(excl, l, kWave);
-            }
-            before += __shfl(incl, 63, kWave);
+    for (int k = 0; k < 2; ++k)
+#pragma unroll
+        for (int i = 0; i < kPer; ++i) {
+            cnt[k][i] = i < per ? hist[k * kBins + tid * per + i] : 0u;
+            tot[k] += cnt[k][i];
         }
-        if (lane == 0 && bin >= 0) {
-            state[k] |= (uint32_t)bin << shift;
-            state[2 + k] = rank - skip;
+    uint32_t incl[2];
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+        incl[k] = tot[k];
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const uint32_t t = __shfl_up(incl[k], o, kWave);
+            if (lane >= o) incl[k] += t;
+        }
+        if (lane == 63) wsum[k][wid] = incl[k];
+    }
+    __syncthreads();  // every thread has read the ranks before any is rewritten
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+        uint32_t run = incl[k] - tot[k];
+        for (int w = 0; w < wid; ++w) run += wsum[k][w];
+        if (run <= rank[k] && rank[k] < run + tot[k]) {
+            bool found = false;
+#pragma unroll
+            for (int i = 0; i < kPer; ++i) {
+                if (found || i >= per) continue;
+                if (rank[k] < run + cnt[k][i]) {
+                    state[k] |= (uint32_t)(tid * per + i) << shift;
+                    state[2 + k] = rank[k] - run;
+                    found = true;
+                } else {
+                    run += cnt[k][i];
+                }
+            }
         }
     }
-    for (int i = lane; i < 2 * kBins; i += 64) hist[i] = 0u;
+#pragma unroll
+    for (int k = 0; k < 2; ++k)
+        for (int i = 0; i < per; ++i) hist[k * kBins + tid * per + i] = 0u;
 }
 
 // P = x_lo + (h - lo) (x_hi - x_lo) in double from the two order statistics; out[0] = P, out[1] = min(cap, P).
@@ -138,13 +200,22 @@ hipError_t launch_calibrate(const void* a, const void* b, int dtype, int d, int6
     const double frac = lo == hi ? 0.0 : h - (double)lo;
     uint32_t* state = scratch;
     uint32_t* hist = scratch + 64;
-    k_pair_cosine<<<dim3((unsigned)((n + 3) / 4)), dim3(256), 0, s>>>(a, b, dtype, d, n, sims);
+    const dim3 pc_grid((unsigned)((n + 3) / 4)), pc_block(256);
+    if (d <= 512)
+        k_pair_cosine<1><<<pc_grid, pc_block, 0, s>>>(a, b, dtype, d, n, sims);
+    else if (d <= 1024)
+        k_pair_cosine<2><<<pc_grid, pc_block, 0, s>>>(a, b, dtype, d, n, sims);
+    else if (d <= 2048)
+        k_pair_cosine<4><<<pc_grid, pc_block, 0, s>>>(a, b, dtype, d, n, sims);
+    else
+        k_pair_cosine<0><<<pc_grid, pc_block, 0, s>>>(a, b, dtype, d, n, sims);
     k_select_init<<<dim3(1), dim3(256), 0, s>>>(state, hist, (uint32_t)lo, (uint32_t)hi);
-    int64_t blocks = (n + 255) / 256;
-    if (blocks > 4 * num_cu) blocks = 4 * num_cu;
+    // at least 16 similarities per thread: each workgroup adds its non-zero bins to the global histogram
+    int64_t blocks = (n + 256 * 16 - 1) / (256 * 16);
+    if (blocks > num_cu) blocks = num_cu;
     for (int pass = 0; pass < kPasses; ++pass) {
         k_select_hist<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(sims, n, pass, state, hist);
-        k_select_scan<<<dim3(1), dim3(64), 0, s>>>(pass, state, hist);
+        k_select_scan<<<dim3(1), dim3(256), 0, s>>>(pass, state, hist);
     }
     k_select_final<<<dim3(1), dim3(64), 0, s>>>(state, frac, cap, tau);
     return hipGetLastError();

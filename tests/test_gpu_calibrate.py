@@ -69,6 +69,48 @@ def _check(lc, c, a, b, p, cap, which=-1, dim=None):
     return sims, tau, o
 
 
+def _lane_order_sims(aq: np.ndarray, bq: np.ndarray) -> np.ndarray:
+    """The float32 dot of two rows of bfloat16 bits in the library's summation order: lane l of a wave takes
+    the columns 512 c + 8 l + e (chunk c, then e = 0..7) in sequence, then the 64 lane sums are combined by a
+    butterfly (x_l += x_(l xor m) for m = 32, 16, .., 1), lane 0's value clamped to [-1, 1].  Products of two
+    bfloat16 values are exact in float32, so the result is fixed bit for bit by the quantised inputs."""
+    n, d = aq.shape
+    nc = max(1, -(-d // 512))
+    def lanes(x):
+        f = np.zeros((n, nc * 512), np.float32)
+        f[:, :d] = (x.astype(np.uint32) << 16).view(np.float32)
+        return f.reshape(n, nc, 64, 8).transpose(0, 2, 1, 3).reshape(n, 64, nc * 8)
+    prod = lanes(aq) * lanes(bq)
+    acc = np.zeros((n, 64), np.float32)
+    for t in range(nc * 8):
+        acc = acc + prod[:, :, t]
+    lane = np.arange(64)
+    for m in (32, 16, 8, 4, 2, 1):
+        acc = acc + acc[:, lane ^ m]
+    return np.clip(acc[:, 0], np.float32(-1), np.float32(1))
+
+
+@pytest.mark.parametrize("in_dtype", [synth.F32, synth.BF16])
+def test_calibration_sims_bit_exact_in_summation_order(lc, in_dtype):
+    """Each pair cosine is the float32 dot of the two vectors quantised exactly as the oracle quantises them
+    (norm in double, one rounding to bfloat16), bit for bit once the summation order is fixed: a single
+    element rounded the other way changes the sum.  Dimensions for every register layout of the kernel
+    (up to 512, 1024 and 2048 columns per row, and beyond)."""
+    rng = np.random.default_rng(71 + in_dtype)
+    for n, d in [(3000, 1), (3000, 200), (3000, 512), (3000, 513), (2000, 1024), (1000, 1500), (1000, 2048),
+                 (500, 2049), (300, 5000)]:
+        say(f"[case] calibrate bit-exact n={n} d={d} dtype={in_dtype}")
+        c = lc.LaCache(10, d, 4, in_dtype, 16, 0)
+        a, b = _pairs(rng, n, d, in_dtype)
+        a[:7] = 0                                     # zero vectors score 0
+        sims, _ = c.calibrate(to_dev(a), to_dev(b), 50.0, 2.0)
+        want = _lane_order_sims(oracle.quantise(a, in_dtype), oracle.quantise(b, in_dtype))
+        got = sims.cpu().numpy()
+        bad = np.nonzero(got != want)[0]
+        assert bad.size == 0, (d, bad[:5], got[bad[:5]], want[bad[:5]])
+        c.close()
+
+
 @pytest.mark.parametrize("in_dtype", [synth.F32, synth.BF16])
 def test_calibration_small_cases(lc, in_dtype):
     rng = np.random.default_rng(61 + in_dtype)
