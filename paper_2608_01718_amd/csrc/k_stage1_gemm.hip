@@ -28,9 +28,9 @@
 // afterwards by replaying the winning group (launch.hpp), which keeps this
 // epilogue branch-free.  The one partial key tile (rows beyond the entry
 // count are zero padding and must not win) is handled by a separate, masked
-// instantiation.  At the end each workgroup writes one packed candidate per
-// query.
-#include <cstdlib>
+// instantiation (a masked epilogue inside the main loop measured 3 % slower:
+// it adds scalar-register pressure to every stage).  At the end each
+// workgroup writes one packed candidate per query.
 #include <type_traits>
 
 #include "common.hpp"
@@ -43,10 +43,7 @@ namespace {
 constexpr int kTile = 256;                           // queries and keys per workgroup tile
 constexpr int kWaves = 8;                            // 2 key halves x 4 query quarters
 constexpr int QF = 2;                                // 32-query MFMA fragments per wave
-#ifndef LACACHE_GEMM_BK
-#define LACACHE_GEMM_BK 64
-#endif
-constexpr int kBK = LACACHE_GEMM_BK;                 // columns of d per LDS stage (32 or 64)
+constexpr int kBK = 64;                              // columns of d per LDS stage (32 measured slower)
 constexpr int kNBuf = 2;                             // LDS stage buffers
 constexpr int kBlk = kBK / 32;                       // 32-column blocks of the tiled layout per stage
 constexpr int kSub = kBK / 16;                       // MFMA k-steps (16 columns) per stage
@@ -282,16 +279,10 @@ hipError_t launch_stage1_gemm(const uint16_t* keys, const uint16_t* qt, int B, i
     if (n_ranges > kMaxPartials - 1) n_ranges = kMaxPartials - 1;
     const int P = n_ranges + (tail ? 1 : 0);
     *P_out = P;
-    // XCD placement: xq query groups x (8 / xq) key parts, when the tile counts divide evenly
-    static const int xq_env = [] {
-        const char* e = std::getenv("LACACHE_GEMM_XQ");
-        return e ? std::atoi(e) : 2;
-    }();
+    // XCD placement: 2 query groups x 4 key parts when the tile counts divide evenly (measured best of 1, 2, 4
+    // and 8 query groups); otherwise plain round-robin
     const int grid = n_qtiles * n_ranges;
-    int xq = 0;
-    if ((xq_env == 1 || xq_env == 2 || xq_env == 4 || xq_env == 8) && n_qtiles % xq_env == 0 &&
-        n_ranges % (8 / xq_env) == 0)
-        xq = xq_env;
+    const int xq = (n_qtiles % 2 == 0 && n_ranges % 4 == 0) ? 2 : 0;
     const size_t lds = (size_t)kNBuf * kStageBytes;
     static bool attr = false;
     if (!attr) {
