@@ -509,7 +509,7 @@ def run_large_interleaved(lc, torch, synth, epochs=8, per_epoch=8, batch=4096):
                 insert_entries_per_s=epochs * batch / (insert_ms * 1e-3),
                 stage1_kernel_avg_ms=k_avg,
                 roofline=dict(bound="mfma", achieved=achieved, peak=PEAK_BF16_TFLOPS, unit="TFLOP/s",
-                              frac=achieved / PEAK_BF16_TFLOPS),
+                              frac=achieved / PEAK_BF16_TFLOPS, traffic=None),
                 rates=rates)
 
 
