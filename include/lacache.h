@@ -190,7 +190,8 @@ int lacache_export_prefix(lacache_t h, int32_t model, int64_t first, int32_t n, 
  * cosines of their response prefixes).
  *   which       -1: the pairs are key-model vectors (dimension d);
  *               0 <= which < m: vectors of prefix model `which` (d_resp[which])
- *   a, b        [n][dim] (cache dtype): pair j is (a[j], b[j]); n >= 1
+ *   a, b        [n][dim] (cache dtype): pair j is (a[j], b[j]);
+ *               1 <= n <= 2^32 - 1 (the selection counts ranks in 32 bits)
  *   percentile  0 .. 100; the percentile is linear between the closest ranks,
  *               h = (n - 1) * percentile / 100, from the order statistics
  *               floor(h) and floor(h) + 1 (computed in double)
@@ -199,7 +200,8 @@ int lacache_export_prefix(lacache_t h, int32_t model, int64_t first, int32_t n, 
  * computes similarities (normalised, bfloat16-rounded vectors, float32 sums,
  * clamped to [-1, 1]); tau [2] float: tau[0] = the percentile of sims,
  * tau[1] = min(cap, tau[0]).  Uses the handle's calibration scratch, so
- * calls on one handle must be ordered on one stream.
+ * calls on one handle must be ordered on one stream.  EINVAL for an invalid
+ * which, n, percentile or cap, or a NULL pointer.
  */
 int lacache_calibrate(lacache_t h, int32_t which, const void *a, const void *b, int64_t n, float percentile,
                       float cap, float *sims, float *tau, void *stream);

@@ -64,57 +64,59 @@ __device__ inline float load_one(const char* row, int dtype, int v) {
 
 }  // namespace
 
+// One workgroup per (query, position) row, grid-stride over the rows.
 __global__ __launch_bounds__(kThreads) void k_token_prob(const void* __restrict__ logits, int dtype, int V,
                                                          const int32_t* __restrict__ tokens, int64_t rows,
                                                          float* __restrict__ p_target) {
-    const int64_t row = blockIdx.x;
-    if (row >= rows) return;
+    __shared__ float sm[kThreads / 64], ss[kThreads / 64];
     const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
     const size_t esz = dtype == 0 ? 4 : 2;
-    const char* r = (const char*)logits + row * (int64_t)V * esz;
-    float m = -__builtin_inff(), s = 0.0f;
-    int tail0 = 0;  // first element not covered by whole aligned chunks
-    if (((uintptr_t)r & 15) == 0) {
-        const int nchunks = V / 8;
-        int c = tid;
-        for (; c + (kUnroll - 1) * kThreads < nchunks; c += kUnroll * kThreads) {
-            float x[kUnroll][8];
+    for (int64_t row = blockIdx.x; row < rows; row += gridDim.x) {
+        const char* r = (const char*)logits + row * (int64_t)V * esz;
+        float m = -__builtin_inff(), s = 0.0f;
+        int tail0 = 0;  // first element not covered by whole aligned chunks
+        if (((uintptr_t)r & 15) == 0) {
+            const int nchunks = V / 8;
+            int c = tid;
+            for (; c + (kUnroll - 1) * kThreads < nchunks; c += kUnroll * kThreads) {
+                float x[kUnroll][8];
 #pragma unroll
-            for (int u = 0; u < kUnroll; ++u) load_chunk(r + (size_t)(c + u * kThreads) * 8 * esz, dtype, x[u]);
+                for (int u = 0; u < kUnroll; ++u) load_chunk(r + (size_t)(c + u * kThreads) * 8 * esz, dtype, x[u]);
 #pragma unroll
-            for (int u = 0; u < kUnroll; ++u) lse_add8(m, s, x[u]);
+                for (int u = 0; u < kUnroll; ++u) lse_add8(m, s, x[u]);
+            }
+            for (; c < nchunks; c += kThreads) {
+                float x[8];
+                load_chunk(r + (size_t)c * 8 * esz, dtype, x);
+                lse_add8(m, s, x);
+            }
+            tail0 = nchunks * 8;
         }
-        for (; c < nchunks; c += kThreads) {
+        for (int v = tail0 + tid; v < V; v += kThreads) {
             float x[8];
-            load_chunk(r + (size_t)c * 8 * esz, dtype, x);
+            x[0] = load_one(r, dtype, v);
+#pragma unroll
+            for (int e = 1; e < 8; ++e) x[e] = -__builtin_inff();
             lse_add8(m, s, x);
         }
-        tail0 = nchunks * 8;
-    }
-    for (int v = tail0 + tid; v < V; v += kThreads) {
-        float x[8];
-        x[0] = load_one(r, dtype, v);
 #pragma unroll
-        for (int e = 1; e < 8; ++e) x[e] = -__builtin_inff();
-        lse_add8(m, s, x);
-    }
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-        const float m2 = __shfl_xor(m, o, kWave), s2 = __shfl_xor(s, o, kWave);
-        lse_merge(m, s, m2, s2);
-    }
-    __shared__ float sm[kThreads / 64], ss[kThreads / 64];
-    if (lane == 0) {
-        sm[wid] = m;
-        ss[wid] = s;
-    }
-    __syncthreads();
-    if (tid == 0) {
-        for (int w = 1; w < kThreads / 64; ++w) lse_merge(m, s, sm[w], ss[w]);
-        const int t = tokens[row];
-        float p = 0.0f;
-        if (t >= 0 && t < V) p = __expf(load_one(r, dtype, t) - m) / s;
-        p_target[row] = p;
+        for (int o = 32; o >= 1; o >>= 1) {
+            const float m2 = __shfl_xor(m, o, kWave), s2 = __shfl_xor(s, o, kWave);
+            lse_merge(m, s, m2, s2);
+        }
+        if (lane == 0) {
+            sm[wid] = m;
+            ss[wid] = s;
+        }
+        __syncthreads();
+        if (tid == 0) {
+            for (int w = 1; w < kThreads / 64; ++w) lse_merge(m, s, sm[w], ss[w]);
+            const int t = tokens[row];
+            float p = 0.0f;
+            if (t >= 0 && t < V) p = __expf(load_one(r, dtype, t) - m) / s;
+            p_target[row] = p;
+        }
+        __syncthreads();  // sm / ss are rewritten by the next row
     }
 }
 
@@ -124,27 +126,29 @@ __global__ __launch_bounds__(256) void k_accept_len(const float* __restrict__ p_
                                                     const float* __restrict__ p_draft, int B, int k,
                                                     int32_t* __restrict__ accept_len) {
     const int lane = threadIdx.x & 63;
-    const int b = blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (b >= B) return;
-    int len = k;
-    for (int j0 = 0; j0 < k; j0 += 64) {
-        const int j = j0 + lane;
-        const bool reject = j < k && !(p_target[(int64_t)b * k + j] >= p_draft[(int64_t)b * k + j]);
-        const uint64_t rej = __ballot(reject);
-        if (rej != 0ull) {
-            len = j0 + __ffsll((unsigned long long)rej) - 1;
-            break;
+    for (int64_t b = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); b < B; b += (int64_t)gridDim.x * 4) {
+        int len = k;
+        for (int j0 = 0; j0 < k; j0 += 64) {
+            const int j = j0 + lane;
+            const bool reject = j < k && !(p_target[b * k + j] >= p_draft[b * k + j]);
+            const uint64_t rej = __ballot(reject);
+            if (rej != 0ull) {
+                len = j0 + __ffsll((unsigned long long)rej) - 1;
+                break;
+            }
         }
+        if (lane == 0) accept_len[b] = len;
     }
-    if (lane == 0) accept_len[b] = len;
 }
 
 hipError_t launch_accept_length(const void* logits, int dtype, int V, const int32_t* tokens, const float* p_draft,
                                 int B, int k, int32_t* accept_len, float* p_target, hipStream_t s) {
     const int64_t rows = (int64_t)B * k;
     if (rows <= 0) return hipSuccess;
-    k_token_prob<<<dim3((unsigned)rows), dim3(kThreads), 0, s>>>(logits, dtype, V, tokens, rows, p_target);
-    k_accept_len<<<dim3((unsigned)((B + 3) / 4)), dim3(256), 0, s>>>(p_target, p_draft, B, k, accept_len);
+    k_token_prob<<<dim3((unsigned)grid_blocks(rows)), dim3(kThreads), 0, s>>>(logits, dtype, V, tokens, rows,
+                                                                              p_target);
+    k_accept_len<<<dim3((unsigned)grid_blocks(((int64_t)B + 3) / 4)), dim3(256), 0, s>>>(p_target, p_draft, B, k,
+                                                                                         accept_len);
     return hipGetLastError();
 }
 

@@ -26,17 +26,15 @@ __constant__ const int kBits[kPasses] = {11, 11, 10};
 
 }  // namespace
 
-// One wave per pair: normalise a[j] and b[j] as stored vectors are, and dot the rounded values in column order
-// per lane, then across the wave.  The rounded values are used as float32 directly (a bfloat16 is a float32
-// with zero low bits); products of two are exact.  NC > 0: d <= 512 NC and each lane keeps its 8 NC columns of
+// One wave per pair (grid-stride over the pairs): normalise a[j] and b[j] as stored vectors are, and dot the
+// rounded values in column order per lane, then across the wave.  The rounded values are used as float32
+// directly (a bfloat16 is a float32 with zero low bits); products of two are exact.  NC > 0: d <= 512 NC and each lane keeps its 8 NC columns of
 // both rows in registers, read once; the norms are summed in the order row_norm uses, so the rounded values
 // are those of the stored vectors.  NC = 0: any d, the rows read once for the norms and once for the dot.
 template <int NC>
-__global__ __launch_bounds__(256) void k_pair_cosine(const void* __restrict__ a, const void* __restrict__ b,
-                                                     int dtype, int d, int64_t n, float* __restrict__ sims) {
+__device__ inline void pair_cosine(const void* __restrict__ a, const void* __restrict__ b, int dtype, int d,
+                                   int64_t j, float* __restrict__ sims) {
     const int lane = threadIdx.x & 63;
-    const int64_t j = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (j >= n) return;
     const size_t esz = dtype == 0 ? 4 : 2;
     const char* ra = (const char*)a + j * d * esz;
     const char* rb = (const char*)b + j * d * esz;
@@ -86,6 +84,13 @@ __global__ __launch_bounds__(256) void k_pair_cosine(const void* __restrict__ a,
     }
     acc = wave_sum_f32(acc);
     if (lane == 0) sims[j] = fminf(fmaxf(acc, -1.0f), 1.0f);
+}
+
+template <int NC>
+__global__ __launch_bounds__(256) void k_pair_cosine(const void* __restrict__ a, const void* __restrict__ b,
+                                                     int dtype, int d, int64_t n, float* __restrict__ sims) {
+    for (int64_t j = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); j < n; j += (int64_t)gridDim.x * 4)
+        pair_cosine<NC>(a, b, dtype, d, j, sims);
 }
 
 // state[0..1]: the key bits found so far for rank 0 / rank 1; state[2..3]: the ranks still to skip inside
@@ -200,7 +205,7 @@ hipError_t launch_calibrate(const void* a, const void* b, int dtype, int d, int6
     const double frac = lo == hi ? 0.0 : h - (double)lo;
     uint32_t* state = scratch;
     uint32_t* hist = scratch + 64;
-    const dim3 pc_grid((unsigned)((n + 3) / 4)), pc_block(256);
+    const dim3 pc_grid((unsigned)grid_blocks((n + 3) / 4)), pc_block(256);
     if (d <= 512)
         k_pair_cosine<1><<<pc_grid, pc_block, 0, s>>>(a, b, dtype, d, n, sims);
     else if (d <= 1024)

@@ -31,49 +31,52 @@ __global__ __launch_bounds__(256) void k_tile_rows(const uint16_t* __restrict__ 
 // the hyperplanes of those words (16 at a time, v_mfma_f32_16x16x32_bf16 with the rows as the row operand; the
 // two 16-hyperplane halves of a word accumulate side by side), packed into sign bits.  Lane l holds, for
 // hyperplane 16 hg + l % 16, the rows 4 (l / 16) + j (j = 0..3); a ballot per j gathers the 16 bits of each
-// row.  Rows outside [row0, row0 + n) are not written.
+// row.  Rows outside [row0, row0 + n) are not written.  Grid-stride over the waves.
 __global__ __launch_bounds__(256) void k_simhash(const u32x4* __restrict__ rows_tiled, int kc, int64_t row0,
                                                  int64_t n, const u32x4* __restrict__ hp_tiled, int bits, int wpw,
                                                  uint32_t* __restrict__ sig) {
     const int lane = threadIdx.x & 63;
     const int words = bits >> 5;
     const int chunks = words / wpw;  // word runs per group
-    const int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-    const int64_t g = (row0 >> 4) + wave / chunks;  // 16-row group
-    const int w0 = (int)(wave % chunks) * wpw;
-    if (g * 16 >= row0 + n) return;
-    const u32x4* a = rows_tiled + g * kc * 64 + lane;
-    for (int w = w0; w < w0 + wpw; ++w) {
-        f32x4 lo = f32x4{0.f, 0.f, 0.f, 0.f}, hi = f32x4{0.f, 0.f, 0.f, 0.f};
-        const u32x4* b0 = hp_tiled + (int64_t)(2 * w) * kc * 64 + lane;
-        const u32x4* b1 = b0 + (int64_t)kc * 64;
-        for (int c = 0; c < kc; c += 4) {  // kc is a multiple of 4: twelve loads in flight per step
-            u32x4 x[4], y0[4], y1[4];
+    // grid-stride over the waves; groups grow with the wave index, so the first one past the rows ends the loop
+    for (int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);; wave += (int64_t)gridDim.x * 4) {
+        const int64_t g = (row0 >> 4) + wave / chunks;  // 16-row group
+        const int w0 = (int)(wave % chunks) * wpw;
+        if (g * 16 >= row0 + n) break;
+        const u32x4* a = rows_tiled + g * kc * 64 + lane;
+        for (int w = w0; w < w0 + wpw; ++w) {
+            f32x4 lo = f32x4{0.f, 0.f, 0.f, 0.f}, hi = f32x4{0.f, 0.f, 0.f, 0.f};
+            const u32x4* b0 = hp_tiled + (int64_t)(2 * w) * kc * 64 + lane;
+            const u32x4* b1 = b0 + (int64_t)kc * 64;
+            for (int c = 0; c < kc; c += 4) {  // kc is a multiple of 4: twelve loads in flight per step
+                u32x4 x[4], y0[4], y1[4];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                x[u] = a[(c + u) * 64];
-                y0[u] = b0[(c + u) * 64];
-                y1[u] = b1[(c + u) * 64];
+                for (int u = 0; u < 4; ++u) {
+                    x[u] = a[(c + u) * 64];
+                    y0[u] = b0[(c + u) * 64];
+                    y1[u] = b1[(c + u) * 64];
+                }
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    lo = mfma16x16x32(x[u], y0[u], lo);
+                    hi = mfma16x16x32(x[u], y1[u], hi);
+                }
             }
+            uint32_t word = 0u;
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                lo = mfma16x16x32(x[u], y0[u], lo);
-                hi = mfma16x16x32(x[u], y1[u], hi);
+            for (int half = 0; half < 2; ++half) {
+                const f32x4 acc = half ? hi : lo;
+                uint64_t m[4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) m[j] = __ballot(acc[j] >= 0.0f);
+                // lane l < 16 owns row 4 (l / 4) + l % 4 = l of the group: its bits sit in m[l % 4] at 16 (l / 4)
+                const uint64_t mine =
+                    (lane & 3) == 0 ? m[0] : (lane & 3) == 1 ? m[1] : (lane & 3) == 2 ? m[2] : m[3];
+                word |= ((uint32_t)(mine >> (16 * ((lane >> 2) & 3))) & 0xFFFFu) << (16 * half);
             }
+            const int64_t row = g * 16 + lane;
+            if (lane < 16 && row >= row0 && row < row0 + n) sig[row * words + w] = word;
         }
-        uint32_t word = 0u;
-#pragma unroll
-        for (int half = 0; half < 2; ++half) {
-            const f32x4 acc = half ? hi : lo;
-            uint64_t m[4];
-#pragma unroll
-            for (int j = 0; j < 4; ++j) m[j] = __ballot(acc[j] >= 0.0f);
-            // lane l < 16 owns row 4 (l / 4) + l % 4 = l of the group: its bits sit in m[l % 4] at 16 (l / 4)
-            const uint64_t mine = (lane & 3) == 0 ? m[0] : (lane & 3) == 1 ? m[1] : (lane & 3) == 2 ? m[2] : m[3];
-            word |= ((uint32_t)(mine >> (16 * ((lane >> 2) & 3))) & 0xFFFFu) << (16 * half);
-        }
-        const int64_t row = g * 16 + lane;
-        if (lane < 16 && row >= row0 && row < row0 + n) sig[row * words + w] = word;
     }
 }
 
@@ -232,7 +235,7 @@ hipError_t launch_simhash(const uint16_t* rows_tiled, int d_pad, int64_t row0, i
     // many rows (building the index): one wave per group, reading its rows once for every word
     const int wpw = (g1 - g0) * words <= 4096 ? 1 : words;
     const int64_t waves = (g1 - g0) * (words / wpw);
-    k_simhash<<<dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, s>>>(
+    k_simhash<<<dim3((unsigned)grid_blocks((waves + 3) / 4)), dim3(256), 0, s>>>(
         (const u32x4*)rows_tiled, d_pad >> 5, row0, n, (const u32x4*)hp_tiled, bits, wpw, sig);
     return hipGetLastError();
 }

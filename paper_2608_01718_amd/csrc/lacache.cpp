@@ -342,8 +342,8 @@ int32_t lacache_models(lacache_t h) { return h ? h->m : -1; }
 
 int lacache_calibrate(lacache_t h, int32_t which, const void* a, const void* b, int64_t n, float percentile, float cap,
                       float* sims, float* tau, void* stream) {
-    if (!h || which < -1 || which >= h->m || n < 1 || !std::isfinite(percentile) || percentile < 0.0f ||
-        percentile > 100.0f || !std::isfinite(cap) || !a || !b || !sims || !tau)
+    if (!h || which < -1 || which >= h->m || n < 1 || n > (int64_t)UINT32_MAX || !std::isfinite(percentile) ||
+        percentile < 0.0f || percentile > 100.0f || !std::isfinite(cap) || !a || !b || !sims || !tau)
         return LACACHE_EINVAL;
     DeviceGuard g(h->device);
     if (!g.ok) return LACACHE_EHIP;

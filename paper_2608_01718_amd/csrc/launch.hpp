@@ -6,6 +6,11 @@
 
 namespace lacache {
 
+// Workgroups of a grid-stride launch: at most 2^20, so that a grid's work-items (blocks x threads, up to
+// 1024 threads) stay far below the 2^32 one dispatch can describe, whatever the row or pair count.
+constexpr int64_t kMaxGridBlocks = int64_t(1) << 20;
+inline int64_t grid_blocks(int64_t want) { return want < 1 ? 1 : (want > kMaxGridBlocks ? kMaxGridBlocks : want); }
+
 // Normalise `rows` input rows (dtype 0 f32 / 1 bf16, row-major [rows][d]) and
 // store them as bfloat16 at destination rows row0 .. row0+rows-1, zero-filling
 // up to rows_pad rows and d_pad columns; `tiled` selects the key layout,
@@ -17,8 +22,8 @@ hipError_t launch_normalise(const void* in, int dtype, int64_t rows, int64_t row
 hipError_t launch_export(const uint16_t* src, int64_t first, int n, int d, int d_pad, uint16_t* dst, bool tiled,
                          hipStream_t s);
 
-// Stage 1, bandwidth-bound path: queries qt (tiled, B <= 64 rows, zero-padded
-// to a multiple of 16) against n_rows tiled keys.  Writes, for every query b
+// Stage 1, bandwidth-bound path: queries qt (tiled; up to 16 * stream_max_qg rows as one group, zero-padded to
+// a multiple of 16, or up to four such groups, zero-padded to whole groups) against n_rows tiled keys.  Writes, for every query b
 // and every workgroup p of the launch, the packed top-1 candidate
 // part[b * P + p] (P <= kMaxPartials).  Returns the number of partials P through *P_out.
 hipError_t launch_stage1_stream(const uint16_t* keys, const uint16_t* qt, int B, int n_rows, int d_pad,

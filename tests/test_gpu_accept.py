@@ -72,6 +72,18 @@ def test_accept_small_shapes(lc, dtype):
         assert exact == B
 
 
+def test_accept_rows_beyond_one_grid(lc):
+    """4.3M queries of one draft token over a 3-token vocabulary: more rows than one launch of either kernel
+    covers (their workgroups and waves loop); a sample of rows from the whole range, including the last."""
+    B, k, V = 4_300_000, 1, 3
+    lg, tok, pd = synth.draft_verification(B, k, V, seed=91, in_dtype=synth.F32)
+    rng = np.random.default_rng(92)
+    rows = np.unique(np.concatenate([rng.integers(0, B, 3000), np.arange(B - 3000, B)]))
+    say(f"[case] accept B={B} k={k} V={V}")
+    _, _, _, exact = _run(lc, lg, synth.F32, tok, pd, rows=rows)
+    assert exact >= rows.size - 10
+
+
 def test_accept_edges(lc):
     import torch
     B, k, V = 6, 9, 515                                        # odd V: bf16 rows are not 16-byte aligned

@@ -111,6 +111,21 @@ def test_calibration_sims_bit_exact_in_summation_order(lc, in_dtype):
         c.close()
 
 
+def test_calibration_pairs_beyond_one_grid(lc):
+    """4.5M pairs: more than one launch of the pair-cosine kernel covers (its waves loop), and a selection over
+    4.5M similarities; pairs from the first and the last stretch bit for bit in the summation order."""
+    rng = np.random.default_rng(81)
+    n, d = 4_500_000, 16
+    a, b = _pairs(rng, n, d, synth.F32)
+    say(f"[case] calibrate n={n} d={d}")
+    c = lc.LaCache(10, d, 4, synth.F32, 16, 0)
+    sims, _, _ = _check(lc, c, a, b, 5.0, 0.8)
+    for sl in (slice(0, 20_000), slice(n - 20_000, n)):
+        want = _lane_order_sims(oracle.quantise(a[sl], synth.F32), oracle.quantise(b[sl], synth.F32))
+        assert np.array_equal(sims[sl], want)
+    c.close()
+
+
 @pytest.mark.parametrize("in_dtype", [synth.F32, synth.BF16])
 def test_calibration_small_cases(lc, in_dtype):
     rng = np.random.default_rng(61 + in_dtype)

@@ -63,6 +63,29 @@ def test_store_matches_oracle_quantisation(lc):
         c.close()
 
 
+def test_single_insert_and_export_beyond_one_grid(lc):
+    """One insert of 4.3M rows (more rows than one launch of the normaliser covers: its waves loop) and one
+    export of all of them (4.3M x 80 values, more than one launch of the export covers: its threads loop),
+    checked against the oracle's quantisation as the store test checks it."""
+    rng = np.random.default_rng(77)
+    N, d = 4_300_000, 80
+    keys = rng.standard_normal((N, d), dtype=np.float32)
+    emb = rng.standard_normal((N, d), dtype=np.float32)
+    tok = rng.integers(0, 1000, (N, 2), dtype=np.int32)
+    say(f"[case] one insert of N={N} d={d} f32, then one export")
+    c = lc.LaCache(N, d, 2, oracle.F32, 16, 0)
+    assert c.insert(to_dev(keys), to_dev(emb), to_dev(tok)) == 0
+    k, e, t = (x.cpu().numpy() for x in c.export(0, N))
+    for got, src in ((k, keys), (e, emb)):
+        want = oracle.quantise(src, oracle.F32)
+        diff = got.view(np.uint16) != want
+        assert diff.mean() <= 1e-3
+        ulp = np.abs(got.view(np.uint16).astype(np.int32) - want.astype(np.int32))
+        assert np.all(ulp[diff] <= 1)
+    np.testing.assert_array_equal(t, tok)
+    c.close()
+
+
 @pytest.mark.parametrize("name", ["tiny", "mid", "mid_paper"])
 def test_parity_full_config(lc, name):
     _run(lc, synth.spec(name))
