@@ -341,9 +341,12 @@ def lacache_accept_length(logits, draft_tokens, p_draft, out=None, stream=None):
     acc, pt = out
     if acc.dtype != torch.int32 or acc.numel() != B or pt.dtype != torch.float32 or pt.numel() != B * k:
         raise ValueError("out: expected (int32 [B], float32 [B, k])")
-    _check(_lib.lacache_accept_length(logits.data_ptr(), dtype, V, draft_tokens.data_ptr(), p_draft.data_ptr(), B, k,
-                                      acc.data_ptr(), pt.data_ptr(), _stream(dev.index, stream)),
-           "lacache_accept_length")
+    if acc.device != dev or pt.device != dev:
+        raise ValueError(f"out: expected tensors on {dev}")
+    with torch.cuda.device(dev):  # the entry point runs on the calling thread's current device
+        _check(_lib.lacache_accept_length(logits.data_ptr(), dtype, V, draft_tokens.data_ptr(), p_draft.data_ptr(),
+                                          B, k, acc.data_ptr(), pt.data_ptr(), _stream(dev.index, stream)),
+               "lacache_accept_length")
     return out
 
 
