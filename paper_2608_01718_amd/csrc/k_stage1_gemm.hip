@@ -284,14 +284,10 @@ hipError_t launch_stage1_gemm(const uint16_t* keys, const uint16_t* qt, int B, i
     const int grid = n_qtiles * n_ranges;
     const int xq = (n_qtiles % 2 == 0 && n_ranges % 4 == 0) ? 2 : 0;
     const size_t lds = (size_t)kNBuf * kStageBytes;
-    static bool attr = false;
-    if (!attr) {
-        (void)hipFuncSetAttribute((const void*)k_stage1_gemm<false>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                  (int)lds);
-        (void)hipFuncSetAttribute((const void*)k_stage1_gemm<true>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                  (int)lds);
-        attr = true;
-    }
+    static std::atomic<uint64_t> lds_full{0}, lds_tail{0};
+    hipError_t e = allow_dynamic_lds((const void*)k_stage1_gemm<false>, (int)lds, lds_full);
+    if (e == hipSuccess) e = allow_dynamic_lds((const void*)k_stage1_gemm<true>, (int)lds, lds_tail);
+    if (e != hipSuccess) return e;
     if (n_ranges > 0)
         k_stage1_gemm<false><<<dim3(grid), dim3(kWaves * 64), lds, s>>>(
             (const u32x4*)keys, (const u32x4*)qt, kc, n_rows, B, n_qtiles, n_full, n_ranges, 0, P, xq, part);

@@ -125,13 +125,9 @@ template <int QG>
 static hipError_t launch_qg(const u32x4* keys, const u32x4* qt, int kc, int groups, int n_rows, int n_ranges,
                             int n_qgroups, int B, uint64_t* part, hipStream_t s) {
     const size_t lds = (size_t)QG * kc * 1024 + (size_t)kStreamWaves * QG * 16 * 8;
-    static bool attr_set = false;
-    if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute((const void*)k_stage1_stream<QG>,
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-        if (e != hipSuccess) return e;
-        attr_set = true;
-    }
+    static std::atomic<uint64_t> lds_allowed{0};
+    const hipError_t e = allow_dynamic_lds((const void*)k_stage1_stream<QG>, 160 * 1024, lds_allowed);
+    if (e != hipSuccess) return e;
     k_stage1_stream<QG><<<dim3(n_ranges * n_qgroups), dim3(kStreamWaves * 64), lds, s>>>(
         keys, qt, kc, groups, n_rows, n_ranges, n_qgroups, B, part);
     return hipGetLastError();

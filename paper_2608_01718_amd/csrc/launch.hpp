@@ -4,12 +4,27 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
+
 namespace lacache {
 
 // Workgroups of a grid-stride launch: at most 2^20, so that a grid's work-items (blocks x threads, up to
 // 1024 threads) stay far below the 2^32 one dispatch can describe, whatever the row or pair count.
 constexpr int64_t kMaxGridBlocks = int64_t(1) << 20;
 inline int64_t grid_blocks(int64_t want) { return want < 1 ? 1 : (want > kMaxGridBlocks ? kMaxGridBlocks : want); }
+
+// Allow kernel `fn` `bytes` of dynamic LDS on the current device, once per device (bit d of `done`; devices
+// past 63 set it on every call).  Safe to call from several threads.
+inline hipError_t allow_dynamic_lds(const void* fn, int bytes, std::atomic<uint64_t>& done) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    const uint64_t bit = dev < 64 ? (uint64_t(1) << dev) : 0;
+    if (bit && (done.load(std::memory_order_acquire) & bit)) return hipSuccess;
+    e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+    if (e == hipSuccess && bit) done.fetch_or(bit, std::memory_order_acq_rel);
+    return e;
+}
 
 // Normalise `rows` input rows (dtype 0 f32 / 1 bf16, row-major [rows][d]) and
 // store them as bfloat16 at destination rows row0 .. row0+rows-1, zero-filling
