@@ -52,6 +52,8 @@ def parse():
     ap.add_argument("--no-calibration", action="store_true", help="skip the threshold-calibration measurement")
     ap.add_argument("--no-accept", action="store_true", help="skip the speculative-decoding acceptance measurement")
     ap.add_argument("--no-lsh", action="store_true", help="skip the LSH-indexed lookup measurement")
+    ap.add_argument("--no-resident", action="store_true",
+                    help="skip the cache-resident workloads (tiny, mid, mid_paper)")
     ap.add_argument("--no-large", action="store_true",
                     help="skip the 4M x 1024 clustered workload with interleaved inserts")
     ap.add_argument("--sweep", action="store_true",
@@ -225,6 +227,21 @@ def run_workload(name, steps, warmup, lc, torch, synth, traffic_db, want_cpu):
     del w, q, a, t, batches
     torch.cuda.empty_cache()
     return res
+
+
+def run_resident(steps, warmup, lc, torch, synth):
+    """The cache-resident workloads, absolute numbers only: tiny (10,000 x 384 float32 input, 64 queries per
+    call) and mid (100,000 x 768 bf16, 256 per call), whose keys (7.7 MB, 154 MB) stay in the 256 MB infinity
+    cache across calls, and the paper-shaped mid_paper (100,000 x 1024, k = 20, thresholds 0.80 / 0.70)."""
+    out = []
+    for name in ("tiny", "mid", "mid_paper"):
+        r = run_workload(name, steps, warmup, lc, torch, synth, {}, False)
+        k_ms = r["roofline"]["kernel_avg_ms"]
+        cfg = r["config"]
+        out.append(dict(workload=cfg["workload"], value=r["value"], unit="lookups/s", ms_per_step=r["ms_per_step"],
+                        stage1_kernel_avg_ms=k_ms, key_read_gbs=cfg["N"] * cfg["d"] * 2 / (k_ms * 1e-3) / 1e9,
+                        rates=r["rates"]))
+    return out
 
 
 def run_ensemble(steps, warmup, lc, torch, synth):
@@ -635,6 +652,7 @@ def main():
     accept = None if args.no_accept else run_accept(args.steps, args.warmup, lc, torch, synth)
     lsh = None if args.no_lsh else run_lsh(args.steps, args.warmup, lc, torch, synth)
     large = None if args.no_large else run_large_interleaved(lc, torch, synth)
+    resident = None if args.no_resident else run_resident(args.steps, args.warmup, lc, torch, synth)
 
     line = {
         "metric": "cache lookups/sec (2-stage) at N=1M,d=768; % HBM / MFMA roofline",
@@ -672,6 +690,8 @@ def main():
         line["lsh"] = lsh
     if large:
         line["large_interleaved"] = large
+    if resident:
+        line["resident"] = resident
     if probe:
         # the same kernels rated against what this GPU sustains: MFMA throughput on random bf16 operands
         # (operand-dependent power lowers the clock below the datasheet's) and a plain streaming read
