@@ -154,11 +154,12 @@ hipError_t launch_stage1_stream(const uint16_t* keys, const uint16_t* qt, int B,
     const int n_qgroups = (B + grp - 1) / grp;
     if (n_qgroups > kStreamMaxGroups) return hipErrorInvalidValue;
     const int qg = n_qgroups == 1 ? (B + 15) / 16 : maxqg;
-    // one workgroup per CU, fewer when there is too little work to give every wave >= 4 groups; with several
-    // query groups a multiple of 8 ranges keeps each range's workgroups on one XCD
+    // one workgroup per CU, fewer when there is too little work to give every wave a 16-key group (small
+    // caches spread over as many CUs as they can: their time is the chain of loads each wave walks); with
+    // several query groups a multiple of 8 ranges keeps each range's workgroups on one XCD
     int cap = num_cu / n_qgroups;
     if (n_qgroups > 1 && cap >= 8) cap = cap / 8 * 8;
-    int n_ranges = (groups + kStreamWaves * 4 - 1) / (kStreamWaves * 4);
+    int n_ranges = (groups + kStreamWaves - 1) / kStreamWaves;
     if (n_ranges > cap) n_ranges = cap;
     if (n_ranges > kMaxPartials) n_ranges = kMaxPartials;
     if (n_ranges < 1) n_ranges = 1;
