@@ -1,9 +1,11 @@
 // roofline_probe.hip -- attainable ceilings of the two bounds the lookup kernels are rated against.
 //
 // A standalone executable (built beside liblacache.so) that prints one JSON line:
-//   mfma_random_tflops    sustained v_mfma_f32_32x32x16_bf16 throughput, operands random bf16 values
-//                         (the data the stage-1 GEMM multiplies);
-//   mfma_constant_tflops  the same loop with constant operands;
+//   mfma_random_tflops    sustained bf16 matrix-core throughput on random bf16 operands (the data the stage-1
+//                         GEMM multiplies): the better of the two forms below;
+//   mfma_random_32x32x16_tflops, mfma_random_16x16x32_tflops  each form alone (v_mfma_f32_32x32x16_bf16, the
+//                         form the GEMM uses, and v_mfma_f32_16x16x32_bf16);
+//   mfma_constant_tflops  the 32x32x16 loop with constant operands;
 //   hbm_read_gbs          best of several passes of two plain streaming reads of a 4 GiB buffer
 //                         (grid-stride, and contiguous per-wave runs).
 // MFMA power depends on the operand bits, so the sustained clock, and with it the matrix-core rate, is lower
@@ -19,6 +21,7 @@ namespace {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 constexpr int kTab = 4096;  // u32x4 entries of the operand table
@@ -49,6 +52,32 @@ __global__ __launch_bounds__(512) void k_mfma(int iters, const u32x4* __restrict
     float s = 0.f;
 #pragma unroll
     for (int i = 0; i < 8; ++i) s += acc[i][lane & 15];
+    out[blockIdx.x * 512 + threadIdx.x] = s;  // keeps every MFMA live
+}
+
+// The same work as k_mfma<true> (random operands) in v_mfma_f32_16x16x32_bf16: half the FLOPs per
+// instruction, so 16 independent accumulators and 32 MFMAs per iteration.
+__global__ __launch_bounds__(512) void k_mfma16(int iters, const u32x4* __restrict__ tab, float* __restrict__ out) {
+    const int lane = threadIdx.x & 63;
+    u32x4 r[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) r[i] = tab[(i * 64 + lane + (int)blockIdx.x * 7) & (kTab - 1)];
+    f32x4 acc[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) acc[i] = f32x4{};
+    for (int it = 0; it < iters; ++it) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+            acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, r[i & 7]),
+                                                             __builtin_bit_cast(bf16x8, r[(i + 3) & 7]), acc[i], 0, 0, 0);
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+            acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, r[(i + 5) & 7]),
+                                                             __builtin_bit_cast(bf16x8, r[(i + 1) & 7]), acc[i], 0, 0, 0);
+    }
+    float s = 0.f;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) s += acc[i][lane & 3];
     out[blockIdx.x * 512 + threadIdx.x] = s;  // keeps every MFMA live
 }
 
@@ -118,14 +147,16 @@ int main() {
     CK(hipEventCreate(&e1));
 
     const int iters = 60000;  // ~50-75 ms per launch: long enough for the clock to settle
-    double tf[2];
-    for (int v = 0; v < 2; ++v) {
+    double tf[3];  // random 32x32x16, constant 32x32x16, random 16x16x32: the same FLOPs each
+    for (int v = 0; v < 3; ++v) {
         float ms = 0.f;
         CK(hipEventRecord(e0));
         if (v == 0)
             k_mfma<true><<<dim3(grid), dim3(512)>>>(iters, tab, out);
-        else
+        else if (v == 1)
             k_mfma<false><<<dim3(grid), dim3(512)>>>(iters, tab, out);
+        else
+            k_mfma16<<<dim3(grid), dim3(512)>>>(iters, tab, out);
         CK(hipGetLastError());
         CK(hipEventRecord(e1));
         CK(hipEventSynchronize(e1));
@@ -161,8 +192,10 @@ int main() {
         const double gbs = moved / (ms * 1e-3) / 1e9;
         if (rep % 6 != 0 && gbs > best_gbs) best_gbs = gbs;
     }
-    printf("{\"mfma_random_tflops\": %.1f, \"mfma_constant_tflops\": %.1f, \"hbm_read_gbs\": %.1f, \"cus\": %d}\n",
-           tf[0], tf[1], best_gbs, ncu);
+    printf("{\"mfma_random_tflops\": %.1f, \"mfma_random_32x32x16_tflops\": %.1f, "
+           "\"mfma_random_16x16x32_tflops\": %.1f, \"mfma_constant_tflops\": %.1f, \"hbm_read_gbs\": %.1f, "
+           "\"cus\": %d}\n",
+           tf[0] > tf[2] ? tf[0] : tf[2], tf[0], tf[2], tf[1], best_gbs, ncu);
     CK(hipFree(tab));
     CK(hipFree(out));
     CK(hipFree(src));
