@@ -134,13 +134,14 @@ __global__ __launch_bounds__(1024) void k_lsh_prep(const void* __restrict__ quer
 
 // Candidates of queries q0 .. q0+nq-1: every entry whose signature differs from the query's in at most `radius`
 // bits is appended to the query's list (at most max_cand kept; cnt counts them all).  Each thread takes
-// kScanKeys entries at a time (the query signatures, in LDS, are read once for all of them).
+// kScanKeys entries at a time (the query signatures, in LDS sized to the nq queries of the launch, are read
+// once for all of them).
 constexpr int kScanKeys = 4;
 __global__ __launch_bounds__(256) void k_lsh_scan(const uint32_t* __restrict__ sig_keys, int64_t n_rows,
                                                   const uint32_t* __restrict__ sig_q, int q0, int nq, int words,
                                                   int radius, int max_cand, uint32_t* __restrict__ cnt,
                                                   int32_t* __restrict__ cand) {
-    __shared__ uint32_t sq[kScanQueries * 8];
+    extern __shared__ uint32_t sq[];  // [nq][words]
     for (int i = threadIdx.x; i < nq * words; i += 256) sq[i] = sig_q[(int64_t)q0 * words + i];
     __syncthreads();
     const int64_t stride = (int64_t)gridDim.x * 256;
@@ -251,13 +252,14 @@ hipError_t launch_lsh_lookup(const void* queries, int dtype, int nb, int d, int 
     if (words < 1 || words > 8) return hipErrorInvalidValue;
     k_lsh_prep<<<dim3((unsigned)((nb + 15) / 16)), dim3(1024), 0, s>>>(queries, dtype, nb, d, d_pad, qt,
                                                                       (const u32x4*)hp_tiled, bits, sigq, cnt);
-    int64_t blocks = (n_rows + 255) / 256;
+    // every thread a whole run of kScanKeys entries (no idle slots), at most 8 workgroups per CU
+    int64_t blocks = (n_rows + 256 * kScanKeys - 1) / (256 * kScanKeys);
     if (blocks > 8 * num_cu) blocks = 8 * num_cu;
     if (blocks < 1) blocks = 1;
     for (int q0 = 0; q0 < nb && n_rows > 0; q0 += kScanQueries) {
         const int nq = nb - q0 < kScanQueries ? nb - q0 : kScanQueries;
-        k_lsh_scan<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(sig_keys, n_rows, sigq, q0, nq, words, radius,
-                                                               max_cand, cnt, cand);
+        k_lsh_scan<<<dim3((unsigned)blocks), dim3(256), (size_t)nq * words * 4, s>>>(
+            sig_keys, n_rows, sigq, q0, nq, words, radius, max_cand, cnt, cand);
     }
     k_lsh_verify<<<dim3((unsigned)((nb + 3) / 4)), dim3(256), 0, s>>>(
         (const u32x4*)keys_tiled, (const u32x4*)qt, d_pad >> 5, nb, cnt, cand, max_cand, n_cand, (int)n_rows,
