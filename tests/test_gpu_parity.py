@@ -252,6 +252,42 @@ def test_determinism_and_paths_agree(lc, B):
     torch.cuda.synchronize()
 
 
+def test_calls_enqueued_on_side_streams(lc):
+    """Inserts and lookups of two independent caches enqueued on two side streams (default priority), with no
+    host synchronisation between the calls: a lookup sees every insert enqueued before it on its stream, and
+    the results equal those of the same calls on the default stream bit for bit."""
+    import torch
+    sp = synth.spec("mid", N=20_000, B=300)
+    w = synth.generate(sp)
+    ref_cache = gpu_cache(lc, sp, w.keys, w.emb, w.tokens)
+    ref = gpu_lookup(ref_cache, w.queries, w.la_emb, w.la_tok, sp.tau_q, sp.tau_r, sp.k)
+    ref_cache.close()
+    keys, emb, tok = to_dev(w.keys), to_dev(w.emb), to_dev(w.tokens)
+    q, a = to_dev(w.queries), to_dev(w.la_emb)
+    t = to_dev(np.ascontiguousarray(w.la_tok[:, :sp.k]))
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    caches, outs = [], []
+    half = sp.N // 2
+    for s in streams:
+        s.wait_stream(torch.cuda.current_stream())
+        c = lc.LaCache(sp.N, sp.d, sp.k_cap, sp.in_dtype, 4096, 0)
+        with torch.cuda.stream(s):
+            assert c.insert(keys[:half], emb[:half], tok[:half], stream=s) == 0
+            assert c.insert(keys[half:], emb[half:], tok[half:], stream=s) == half
+            outs.append(c.lookup(q, a, t, sp.tau_q, sp.tau_r, sp.k, stream=s))
+        caches.append(c)
+    for s in streams:
+        s.synchronize()
+    for out in outs:
+        g = dict(zip(("idx", "score", "resp_score", "decision"), (x.cpu().numpy() for x in out)))
+        for name in ("idx", "decision"):
+            np.testing.assert_array_equal(g[name], ref[name])
+        for name in ("score", "resp_score"):
+            np.testing.assert_array_equal(g[name].view(np.uint32), ref[name].view(np.uint32))
+    for c in caches:
+        c.close()
+
+
 def test_interleaved_inserts(lc):
     """A query planted near an entry is a miss before that entry is inserted and a hit after it."""
     sp = synth.spec("large", N=12_288, B=256)
