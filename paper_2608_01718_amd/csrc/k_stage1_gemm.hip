@@ -25,7 +25,7 @@
 // four 32-row groups and keeps a running (best score, 32-row group); only a
 // strictly larger score replaces the best and the lowest group wins within a
 // tile, so ties keep the lowest group.  The exact lowest row is recovered
-// afterwards by replaying the winning group (launch.hpp), which keeps this
+// afterwards by replaying the winning group (verify.hpp), which keeps this
 // epilogue branch-free.  The one partial key tile (rows beyond the entry
 // count are zero padding and must not win) is handled by a separate, masked
 // instantiation (a masked epilogue inside the main loop measured 3 % slower:
@@ -110,7 +110,7 @@ __global__ __launch_bounds__(512, 1) void k_stage1_gemm(const u32x4* __restrict_
     const int T = (kt1 - kt0) * spt;          // stages of the whole range
 
     // running best of each lane per 32-query fragment b: the score, and the 32-row group (global row / 32)
-    // holding it -- the exact row is recovered later by replaying that group (see launch.hpp)
+    // holding it -- the exact row is recovered later by replaying that group (verify.hpp)
     float best[QF];
     int bgrp[QF];
 #pragma unroll
