@@ -32,7 +32,7 @@ __constant__ const int kBits[kPasses] = {11, 11, 10};
 // both rows in registers, read once; the norms are summed in the order row_norm uses, so the rounded values
 // are those of the stored vectors.  NC = 0: any d, the rows read once for the norms and once for the dot.
 template <int NC>
-__device__ inline void pair_cosine(const void* __restrict__ a, const void* __restrict__ b, int dtype, int d,
+__device__ __forceinline__ void pair_cosine(const void* __restrict__ a, const void* __restrict__ b, int dtype, int d,
                                    int64_t j, float* __restrict__ sims) {
     const int lane = threadIdx.x & 63;
     const size_t esz = dtype == 0 ? 4 : 2;
@@ -86,11 +86,18 @@ __device__ inline void pair_cosine(const void* __restrict__ a, const void* __res
     if (lane == 0) sims[j] = fminf(fmaxf(acc, -1.0f), 1.0f);
 }
 
-template <int NC>
+// LOOP: grid-stride over the pairs, for more pairs than one grid holds; else one pair per wave (the loop's
+// carried state costs registers, and with them occupancy, on this latency-bound kernel).
+template <int NC, bool LOOP>
 __global__ __launch_bounds__(256) void k_pair_cosine(const void* __restrict__ a, const void* __restrict__ b,
                                                      int dtype, int d, int64_t n, float* __restrict__ sims) {
-    for (int64_t j = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); j < n; j += (int64_t)gridDim.x * 4)
-        pair_cosine<NC>(a, b, dtype, d, j, sims);
+    const int64_t j0 = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if constexpr (LOOP) {
+        for (int64_t j = j0; j < n; j += (int64_t)gridDim.x * 4) pair_cosine<NC>(a, b, dtype, d, j, sims);
+    } else {
+        if (j0 >= n) return;
+        pair_cosine<NC>(a, b, dtype, d, j0, sims);
+    }
 }
 
 // state[0..1]: the key bits found so far for rank 0 / rank 1; state[2..3]: the ranks still to skip inside
@@ -206,14 +213,25 @@ hipError_t launch_calibrate(const void* a, const void* b, int dtype, int d, int6
     uint32_t* state = scratch;
     uint32_t* hist = scratch + 64;
     const dim3 pc_grid((unsigned)grid_blocks((n + 3) / 4)), pc_block(256);
-    if (d <= 512)
-        k_pair_cosine<1><<<pc_grid, pc_block, 0, s>>>(a, b, dtype, d, n, sims);
-    else if (d <= 1024)
-        k_pair_cosine<2><<<pc_grid, pc_block, 0, s>>>(a, b, dtype, d, n, sims);
-    else if (d <= 2048)
-        k_pair_cosine<4><<<pc_grid, pc_block, 0, s>>>(a, b, dtype, d, n, sims);
-    else
-        k_pair_cosine<0><<<pc_grid, pc_block, 0, s>>>(a, b, dtype, d, n, sims);
+    if ((n + 3) / 4 > kMaxGridBlocks) {
+        if (d <= 512)
+            k_pair_cosine<1, true><<<pc_grid, pc_block, 0, s>>>(a, b, dtype, d, n, sims);
+        else if (d <= 1024)
+            k_pair_cosine<2, true><<<pc_grid, pc_block, 0, s>>>(a, b, dtype, d, n, sims);
+        else if (d <= 2048)
+            k_pair_cosine<4, true><<<pc_grid, pc_block, 0, s>>>(a, b, dtype, d, n, sims);
+        else
+            k_pair_cosine<0, true><<<pc_grid, pc_block, 0, s>>>(a, b, dtype, d, n, sims);
+    } else {
+        if (d <= 512)
+            k_pair_cosine<1, false><<<pc_grid, pc_block, 0, s>>>(a, b, dtype, d, n, sims);
+        else if (d <= 1024)
+            k_pair_cosine<2, false><<<pc_grid, pc_block, 0, s>>>(a, b, dtype, d, n, sims);
+        else if (d <= 2048)
+            k_pair_cosine<4, false><<<pc_grid, pc_block, 0, s>>>(a, b, dtype, d, n, sims);
+        else
+            k_pair_cosine<0, false><<<pc_grid, pc_block, 0, s>>>(a, b, dtype, d, n, sims);
+    }
     k_select_init<<<dim3(1), dim3(256), 0, s>>>(state, hist, (uint32_t)lo, (uint32_t)hi);
     // at least 16 similarities per thread: each workgroup adds its non-zero bins to the global histogram
     int64_t blocks = (n + 256 * 16 - 1) / (256 * 16);
