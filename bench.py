@@ -187,6 +187,15 @@ def run_workload(name, steps, warmup, lc, torch, synth, traffic_db, want_cpu):
     e1.record()
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / steps
+    # per-call times (median and minimum) from a pass with events around every call
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for i in range(steps):
+        ev[i][0].record()
+        step(i)
+        ev[i][1].record()
+    torch.cuda.synchronize()
+    per_call = sorted(a.elapsed_time(b) for a, b in ev)
+    call_ms = dict(median=per_call[len(per_call) // 2], min=per_call[0])
     # a second pass of the same steps with the library's stage-1 events on
     c.profile(True)
     for i in range(steps):
@@ -218,7 +227,7 @@ def run_workload(name, steps, warmup, lc, torch, synth, traffic_db, want_cpu):
     # counters describe the code they were taken on: a changed kernel reports no traffic
     roof["traffic"] = t["traffic_bytes"] if t and t.get("sources_digest") == sources_digest(name) else None
     roof["kernel_avg_ms"] = k_avg
-    res = dict(workload=name, value=call_b / (ms * 1e-3), unit="lookups/s", ms_per_step=ms, B=call_b,
+    res = dict(workload=name, value=call_b / (ms * 1e-3), unit="lookups/s", ms_per_step=ms, B=call_b, call_ms=call_ms,
                roofline=roof, rates=rates, config=dict(workload=describe(sp, call_b), N=sp.N, d=sp.d, B=call_b,
                                                        k=sp.k, k_cap=sp.k_cap, tau_q=sp.tau_q, tau_r=sp.tau_r))
     if want_cpu:
@@ -670,6 +679,7 @@ def main():
         "config": main_res["config"],
         "roofline": {k: main_res["roofline"][k] for k in ("bound", "achieved", "peak", "unit", "frac", "traffic")},
         "stage1_kernel_avg_ms": main_res["roofline"]["kernel_avg_ms"],
+        "call_ms": main_res["call_ms"],
         "rates": main_res["rates"],
         "cpu_baseline": main_res.get("cpu_baseline"),
     }
@@ -679,7 +689,8 @@ def main():
             "ms_per_step": secondary["ms_per_step"],
             "roofline": {k: secondary["roofline"][k] for k in ("bound", "achieved", "peak", "unit", "frac",
                                                                   "traffic")},
-            "stage1_kernel_avg_ms": secondary["roofline"]["kernel_avg_ms"], "rates": secondary["rates"]}
+            "stage1_kernel_avg_ms": secondary["roofline"]["kernel_avg_ms"], "call_ms": secondary["call_ms"],
+            "rates": secondary["rates"]}
     if ensemble:
         line["ensemble"] = ensemble
     if calibration:
