@@ -71,6 +71,7 @@ def lib():
                                      P, P]
         L.lco_first_identical.restype = i64
         L.lco_num_threads.restype = ctypes.c_int
+        L.lco_set_num_threads.argtypes = [ctypes.c_int]
         L.lco_lookup_ensemble.argtypes = [P, i64, i32, P, i32, f32, i32, P, P, P, P, P, i32, P, i32, P, P, P, P]
         _lib = L
     return _lib
@@ -263,6 +264,11 @@ def lookup_lsh(keys_q, emb_q, tokens, sig_keys, q_q, sig_q, a_q, u, radius: int,
 def num_threads() -> int:
     """Threads the oracle's parallel loops use."""
     return int(lib().lco_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """Threads the oracle's parallel loops use from now on (n >= 1)."""
+    lib().lco_set_num_threads(int(n))
 
 
 def first_identical(keys_q, i: int) -> int:

@@ -289,6 +289,13 @@ void lco_bf16_rne_array(const double *in, int64_t n, uint16_t *out)
         out[i] = lco_bf16_rne(in[i]);
 }
 
+/* Threads the following parallel regions use (n >= 1); for timing the oracle on one thread. */
+void lco_set_num_threads(int n)
+{
+    if (n >= 1)
+        omp_set_num_threads(n);
+}
+
 /* Threads an OpenMP parallel region of the oracle uses (reported beside its timings). */
 int lco_num_threads(void)
 {
