@@ -78,11 +78,17 @@ STAGE1_SOURCES = {"serve_large": ["k_stage1_gemm.hip", "common.hpp"],
 
 
 def sources_digest(name):
-    """Digest of the sources of a workload's stage-1 kernel: counters are valid only for that code."""
+    """Digest of the sources of a workload's stage-1 kernel: counters are valid only for that code.  Comments
+    and runs of white space are left out, so editing a comment keeps the counters; any change to the code
+    voids them."""
     import hashlib
+    import re
     h = hashlib.sha256()
     for f in STAGE1_SOURCES[name]:
-        h.update(open(os.path.join(ROOT, "paper_2608_01718_amd", "csrc", f), "rb").read())
+        text = open(os.path.join(ROOT, "paper_2608_01718_amd", "csrc", f)).read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()[:16]
 
 
