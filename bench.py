@@ -726,7 +726,8 @@ def main():
         att = {"mfma_bf16_random_tflops": probe["mfma_random_tflops"],
                "mfma_bf16_random_32x32x16_tflops": probe.get("mfma_random_32x32x16_tflops"),
                "mfma_bf16_random_16x16x32_tflops": probe.get("mfma_random_16x16x32_tflops"),
-               "mfma_bf16_constant_tflops": probe["mfma_constant_tflops"], "hbm_read_gbs": probe["hbm_read_gbs"]}
+               "mfma_bf16_constant_tflops": probe["mfma_constant_tflops"], "hbm_read_gbs": probe["hbm_read_gbs"],
+               "hbm_read_plain_gbs": probe.get("hbm_read_plain_gbs")}
         for key, res in (("frac", main_res), ("secondary_frac", secondary)):
             if not res:
                 continue

@@ -9,7 +9,7 @@
 // running (maximum, sum of exponentials relative to it) per thread over
 // 16-byte chunks of the row, merges the pairs across the workgroup, and
 // divides the token's exponential by the sum.  The kernel is bound by reading
-// the logits.  A second kernel finds, per query, the first rejected position
+// the logits, which it reads once, with non-temporal loads.  A second kernel finds, per query, the first rejected position
 // with a wave ballot.
 #include "common.hpp"
 #include "launch.hpp"
@@ -43,17 +43,21 @@ __device__ inline void lse_add8(float& m, float& s, const float x[8]) {
     for (int e = 0; e < 8; ++e) s += __expf(x[e] - m);
 }
 
+// 8 logits from 16-byte aligned memory, by non-temporal loads (each logit is read once)
 __device__ inline void load_chunk(const char* p, int dtype, float x[8]) {
     if (dtype == 0) {
-        const float4 a = ((const float4*)p)[0], b = ((const float4*)p)[1];
-        x[0] = a.x, x[1] = a.y, x[2] = a.z, x[3] = a.w, x[4] = b.x, x[5] = b.y, x[6] = b.z, x[7] = b.w;
-    } else {
-        const uint4 a = *(const uint4*)p;
-        const uint32_t w[4] = {a.x, a.y, a.z, a.w};
+        const u32x4 a = __builtin_nontemporal_load((const u32x4*)p), b = __builtin_nontemporal_load((const u32x4*)p + 1);
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
-            x[2 * t] = __uint_as_float(w[t] << 16);
-            x[2 * t + 1] = __uint_as_float(w[t] & 0xFFFF0000u);
+            x[t] = __uint_as_float(a[t]);
+            x[4 + t] = __uint_as_float(b[t]);
+        }
+    } else {
+        const u32x4 a = __builtin_nontemporal_load((const u32x4*)p);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            x[2 * t] = __uint_as_float(a[t] << 16);
+            x[2 * t + 1] = __uint_as_float(a[t] & 0xFFFF0000u);
         }
     }
 }

@@ -6,8 +6,9 @@
 //   mfma_random_32x32x16_tflops, mfma_random_16x16x32_tflops  each form alone (v_mfma_f32_32x32x16_bf16, the
 //                         form the GEMM uses, and v_mfma_f32_16x16x32_bf16);
 //   mfma_constant_tflops  the 32x32x16 loop with constant operands;
-//   hbm_read_gbs          best of several passes of two plain streaming reads of a 4 GiB buffer
-//                         (grid-stride, and contiguous per-wave runs).
+//   hbm_read_gbs          best of several passes of three streaming reads of a 4 GiB buffer (grid-stride,
+//                         contiguous per-wave runs, and the runs with non-temporal loads);
+//   hbm_read_plain_gbs    the best of the two with plain loads.
 // MFMA power depends on the operand bits, so the sustained clock, and with it the matrix-core rate, is lower
 // for random data than for constant data; the datasheet peak assumes the maximum clock.
 #include <hip/hip_runtime.h>
@@ -95,7 +96,9 @@ __global__ __launch_bounds__(256) void k_read(const u32x4* __restrict__ src, int
 }
 
 // Contiguous per-wave runs: wave w of the grid reads words [w * per_wave, (w + 1) * per_wave) as 1 KiB
-// coalesced wave loads, eight in flight (per_wave is a multiple of 512 words).
+// coalesced wave loads, eight in flight (per_wave is a multiple of 512 words).  NT: non-temporal loads (the
+// data is not kept in the caches), as the streaming stage-1 kernel reads its keys.
+template <bool NT>
 __global__ __launch_bounds__(1024) void k_read_runs(const u32x4* __restrict__ src, int64_t per_wave,
                                                     u32x4* __restrict__ out) {
     const int lane = threadIdx.x & 63;
@@ -105,7 +108,7 @@ __global__ __launch_bounds__(1024) void k_read_runs(const u32x4* __restrict__ sr
     for (int64_t j = 0; j < per_wave; j += 512) {
         u32x4 v[8];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) v[u] = p[j + u * 64];
+        for (int u = 0; u < 8; ++u) v[u] = NT ? __builtin_nontemporal_load(p + j + u * 64) : p[j + u * 64];
 #pragma unroll
         for (int u = 0; u < 8; ++u) x ^= v[u];
     }
@@ -175,27 +178,31 @@ int main() {
     // runs: 2 workgroups of 16 waves per CU; words per wave rounded down to whole 8 KiB steps
     const int run_grid = 2 * ncu, run_waves = run_grid * 16;
     const int64_t per_wave = n / run_waves / 512 * 512;
-    double best_gbs = 0.0;
-    for (int rep = 0; rep < 12; ++rep) {
+    double best_gbs = 0.0, best_plain = 0.0;
+    for (int rep = 0; rep < 18; ++rep) {
         float ms = 0.f;
-        const bool runs = rep >= 6;
+        const int kind = rep / 6;  // 0 grid-stride, 1 runs, 2 runs with non-temporal loads
         CK(hipEventRecord(e0));
-        if (runs)
-            k_read_runs<<<dim3(run_grid), dim3(1024)>>>(src, per_wave, sink);
-        else
+        if (kind == 0)
             k_read<<<dim3(rgrid), dim3(256)>>>(src, n, sink);
+        else if (kind == 1)
+            k_read_runs<false><<<dim3(run_grid), dim3(1024)>>>(src, per_wave, sink);
+        else
+            k_read_runs<true><<<dim3(run_grid), dim3(1024)>>>(src, per_wave, sink);
         CK(hipGetLastError());
         CK(hipEventRecord(e1));
         CK(hipEventSynchronize(e1));
         CK(hipEventElapsedTime(&ms, e0, e1));
-        const double moved = runs ? (double)per_wave * run_waves * 16 : (double)bytes;
+        const double moved = kind ? (double)per_wave * run_waves * 16 : (double)bytes;
         const double gbs = moved / (ms * 1e-3) / 1e9;
-        if (rep % 6 != 0 && gbs > best_gbs) best_gbs = gbs;
+        if (rep % 6 == 0) continue;  // the first pass of each kind warms up
+        if (gbs > best_gbs) best_gbs = gbs;
+        if (kind < 2 && gbs > best_plain) best_plain = gbs;
     }
     printf("{\"mfma_random_tflops\": %.1f, \"mfma_random_32x32x16_tflops\": %.1f, "
            "\"mfma_random_16x16x32_tflops\": %.1f, \"mfma_constant_tflops\": %.1f, \"hbm_read_gbs\": %.1f, "
-           "\"cus\": %d}\n",
-           tf[0] > tf[2] ? tf[0] : tf[2], tf[0], tf[2], tf[1], best_gbs, ncu);
+           "\"hbm_read_plain_gbs\": %.1f, \"cus\": %d}\n",
+           tf[0] > tf[2] ? tf[0] : tf[2], tf[0], tf[2], tf[1], best_gbs, best_plain, ncu);
     CK(hipFree(tab));
     CK(hipFree(out));
     CK(hipFree(src));
