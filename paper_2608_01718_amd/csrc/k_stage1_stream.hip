@@ -7,8 +7,8 @@
 // reading the keys once: every wave streams a contiguous run of 16-key groups
 // (d_pad*32 contiguous bytes each) with 1 KiB coalesced non-temporal loads
 // (read once, they are not kept in the caches: ~13 % more read bandwidth than
-// plain loads), double buffered, while the queries sit in LDS for the whole
-// launch.  Larger
+// plain loads; plain loads when several query groups share the range), double
+// buffered, while the queries sit in LDS for the whole launch.  Larger
 // batches run as up to four 64-query groups: the workgroups of one key range
 // sit on the same XCD and start together, so the range comes from HBM once
 // and the other readers find it in that XCD's L2 (or the infinity cache).
@@ -25,7 +25,9 @@ namespace lacache {
 constexpr int kStreamWaves = 16;     // waves per workgroup; one workgroup per CU
 constexpr int kStreamMaxGroups = 4;  // query groups of one launch, each reading every key range
 
-template <int QG>
+// NT: the keys are loaded non-temporally (one query group: each key range has a single reader); with several
+// query groups plain loads keep a range in L2 for the other groups' workgroups.
+template <int QG, bool NT>
 __global__ __launch_bounds__(1024) void k_stage1_stream(const u32x4* __restrict__ keys, const u32x4* __restrict__ qt,
                                                         int kc, int groups, int n_rows, int n_ranges, int n_qgroups,
                                                         int B, uint64_t* __restrict__ part) {
@@ -67,7 +69,7 @@ __global__ __launch_bounds__(1024) void k_stage1_stream(const u32x4* __restrict_
     u32x4 cur[4], nxt[4];
     if (nchunks > 0) {
 #pragma unroll
-        for (int u = 0; u < 4; ++u) cur[u] = __builtin_nontemporal_load(kp + u * 64);
+        for (int u = 0; u < 4; ++u) cur[u] = NT ? __builtin_nontemporal_load(kp + u * 64) : kp[u * 64];
     }
     f32x4 acc[QG];
 #pragma unroll
@@ -76,7 +78,10 @@ __global__ __launch_bounds__(1024) void k_stage1_stream(const u32x4* __restrict_
     for (int c = 0; c < nchunks; c += 4) {
         if (c + 4 < nchunks) {
 #pragma unroll
-            for (int u = 0; u < 4; ++u) nxt[u] = __builtin_nontemporal_load(kp + (int64_t)(c + 4 + u) * 64);
+            for (int u = 0; u < 4; ++u) {
+                const u32x4* a = kp + (int64_t)(c + 4 + u) * 64;
+                nxt[u] = NT ? __builtin_nontemporal_load(a) : *a;
+            }
         }
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
@@ -123,14 +128,14 @@ __global__ __launch_bounds__(1024) void k_stage1_stream(const u32x4* __restrict_
     }
 }
 
-template <int QG>
+template <int QG, bool NT>
 static hipError_t launch_qg(const u32x4* keys, const u32x4* qt, int kc, int groups, int n_rows, int n_ranges,
                             int n_qgroups, int B, uint64_t* part, hipStream_t s) {
     const size_t lds = (size_t)QG * kc * 1024 + (size_t)kStreamWaves * QG * 16 * 8;
     static std::atomic<uint64_t> lds_allowed{0};
-    const hipError_t e = allow_dynamic_lds((const void*)k_stage1_stream<QG>, 160 * 1024, lds_allowed);
+    const hipError_t e = allow_dynamic_lds((const void*)k_stage1_stream<QG, NT>, 160 * 1024, lds_allowed);
     if (e != hipSuccess) return e;
-    k_stage1_stream<QG><<<dim3(n_ranges * n_qgroups), dim3(kStreamWaves * 64), lds, s>>>(
+    k_stage1_stream<QG, NT><<<dim3(n_ranges * n_qgroups), dim3(kStreamWaves * 64), lds, s>>>(
         keys, qt, kc, groups, n_rows, n_ranges, n_qgroups, B, part);
     return hipGetLastError();
 }
@@ -169,10 +174,18 @@ hipError_t launch_stage1_stream(const uint16_t* keys, const uint16_t* qt, int B,
     const u32x4* k4 = (const u32x4*)keys;
     const u32x4* q4 = (const u32x4*)qt;
     switch (qg) {
-        case 1: return launch_qg<1>(k4, q4, kc, groups, n_rows, n_ranges, n_qgroups, B, part, s);
-        case 2: return launch_qg<2>(k4, q4, kc, groups, n_rows, n_ranges, n_qgroups, B, part, s);
-        case 3: return launch_qg<3>(k4, q4, kc, groups, n_rows, n_ranges, n_qgroups, B, part, s);
-        default: return launch_qg<4>(k4, q4, kc, groups, n_rows, n_ranges, n_qgroups, B, part, s);
+        case 1:
+            return n_qgroups == 1 ? launch_qg<1, true>(k4, q4, kc, groups, n_rows, n_ranges, n_qgroups, B, part, s)
+                                  : launch_qg<1, false>(k4, q4, kc, groups, n_rows, n_ranges, n_qgroups, B, part, s);
+        case 2:
+            return n_qgroups == 1 ? launch_qg<2, true>(k4, q4, kc, groups, n_rows, n_ranges, n_qgroups, B, part, s)
+                                  : launch_qg<2, false>(k4, q4, kc, groups, n_rows, n_ranges, n_qgroups, B, part, s);
+        case 3:
+            return n_qgroups == 1 ? launch_qg<3, true>(k4, q4, kc, groups, n_rows, n_ranges, n_qgroups, B, part, s)
+                                  : launch_qg<3, false>(k4, q4, kc, groups, n_rows, n_ranges, n_qgroups, B, part, s);
+        default:
+            return n_qgroups == 1 ? launch_qg<4, true>(k4, q4, kc, groups, n_rows, n_ranges, n_qgroups, B, part, s)
+                                  : launch_qg<4, false>(k4, q4, kc, groups, n_rows, n_ranges, n_qgroups, B, part, s);
     }
 }
 
