@@ -155,6 +155,41 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+def sclk_under_load(torch, step, seconds=1.5):
+    """The GPU's shader clock (MHz) while `step` runs back to back: rocm-smi is sampled once, from a separate
+    thread, half a second into ~`seconds` of continuous calls.  None when the tool or its reading is missing."""
+    import re
+    import shutil
+    import subprocess
+    import threading
+    smi = shutil.which("rocm-smi")
+    if smi is None:
+        return None
+    got = {}
+
+    def sample():
+        time.sleep(0.5)
+        try:
+            r = subprocess.run([smi, "--showclocks", "--json"], capture_output=True, text=True, timeout=20)
+            m = re.search(r"sclk clock speed:\"\s*:\s*\"\((\d+)Mhz\)", r.stdout)
+            got["mhz"] = int(m.group(1)) if m else None
+        except (OSError, subprocess.SubprocessError):
+            got["mhz"] = None
+
+    th = threading.Thread(target=sample)
+    t0 = time.time()
+    th.start()
+    i = 0
+    while th.is_alive() or time.time() - t0 < seconds:
+        step(i)
+        i += 1
+        if i % 16 == 0:
+            torch.cuda.synchronize()
+    torch.cuda.synchronize()
+    th.join()
+    return got.get("mhz")
+
+
 def describe(sp, call_b):
     return (f"{sp.name}: N={sp.N:,} cached entries, d={sp.d} bf16 keys and prefix embeddings, k={sp.k} prefix "
             f"tokens, vocab {sp.vocab}, B={call_b} queries per call "
@@ -202,6 +237,7 @@ def run_workload(name, steps, warmup, lc, torch, synth, traffic_db, want_cpu):
     torch.cuda.synchronize()
     per_call = sorted(a.elapsed_time(b) for a, b in ev)
     call_ms = dict(median=per_call[len(per_call) // 2], min=per_call[0])
+    sclk = sclk_under_load(torch, step)
     # a second pass of the same steps with the library's stage-1 events on
     c.profile(True)
     for i in range(steps):
@@ -234,6 +270,7 @@ def run_workload(name, steps, warmup, lc, torch, synth, traffic_db, want_cpu):
     roof["traffic"] = t["traffic_bytes"] if t and t.get("sources_digest") == sources_digest(name) else None
     roof["kernel_avg_ms"] = k_avg
     res = dict(workload=name, value=call_b / (ms * 1e-3), unit="lookups/s", ms_per_step=ms, B=call_b, call_ms=call_ms,
+               sclk_mhz=sclk,
                roofline=roof, rates=rates, config=dict(workload=describe(sp, call_b), N=sp.N, d=sp.d, B=call_b,
                                                        k=sp.k, k_cap=sp.k_cap, tau_q=sp.tau_q, tau_r=sp.tau_r))
     if want_cpu:
@@ -697,6 +734,7 @@ def main():
         "roofline": {k: main_res["roofline"][k] for k in ("bound", "achieved", "peak", "unit", "frac", "traffic")},
         "stage1_kernel_avg_ms": main_res["roofline"]["kernel_avg_ms"],
         "call_ms": main_res["call_ms"],
+        "sclk_mhz_under_load": main_res["sclk_mhz"],
         "rates": main_res["rates"],
         "cpu_baseline": main_res.get("cpu_baseline"),
     }
@@ -707,6 +745,7 @@ def main():
             "roofline": {k: secondary["roofline"][k] for k in ("bound", "achieved", "peak", "unit", "frac",
                                                                   "traffic")},
             "stage1_kernel_avg_ms": secondary["roofline"]["kernel_avg_ms"], "call_ms": secondary["call_ms"],
+            "sclk_mhz_under_load": secondary["sclk_mhz"],
             "rates": secondary["rates"]}
     if ensemble:
         line["ensemble"] = ensemble
