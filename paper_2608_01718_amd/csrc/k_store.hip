@@ -28,6 +28,43 @@ __global__ __launch_bounds__(256) void k_normalise_rows(const void* __restrict__
     }
 }
 
+// The tiled layout (keys, staged queries), one workgroup of 4 waves per 16-row group of the destination
+// (grid-stride over the groups): the waves first take the norms of the group's rows (row_norm, as above),
+// then each wave writes whole 1 KiB chunks -- lane l holds row l % 16, columns 8 (l / 16) .. +7 of the chunk --
+// so every store is one contiguous wave access.  Destination rows outside [row0, row0 + rows_pad) belong
+// to other calls and are not written; rows >= rows are written as zeros.
+__global__ __launch_bounds__(256) void k_normalise_tiled(const void* __restrict__ in, int dtype, int64_t rows,
+                                                         int64_t rows_pad, int d, int d_pad,
+                                                         uint16_t* __restrict__ out, int64_t row0) {
+    __shared__ double norms[16];
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+    const int kc = d_pad >> 5;
+    const size_t esz = dtype == 0 ? 4 : 2;
+    const int64_t g0 = row0 >> 4, g1 = (row0 + rows_pad + 15) >> 4;
+    for (int64_t g = g0 + blockIdx.x; g < g1; g += gridDim.x) {
+        const int64_t r_first = g * 16 - row0;  // call row of the group's row 0
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int i = wid * 4 + k;
+            const int64_t r = r_first + i;
+            const bool live = r >= 0 && r < rows;
+            const double n = row_norm((const char*)in + (live ? r * (int64_t)d * esz : 0), dtype, d, live, lane);
+            if (lane == 0) norms[i] = n;
+        }
+        __syncthreads();
+        const int i = lane & 15;
+        const int64_t r = r_first + i;
+        const bool live = r >= 0 && r < rows;
+        const bool mine = r >= 0 && r < rows_pad;
+        const char* src = (const char*)in + (live ? r * (int64_t)d * esz : 0);
+        for (int c = wid; c < kc; c += 4) {
+            const u32x4 w = quantise8(src, dtype, d, c * 32 + 8 * (lane >> 4), norms[i], live);
+            if (mine) *(u32x4*)(out + ((g * kc + c) * 64 + lane) * 8) = w;
+        }
+        __syncthreads();  // norms[] is rewritten by the next group
+    }
+}
+
 // Copy rows first .. first+n-1 of a bfloat16 matrix (tiled or row-major with
 // d_pad columns) into a dense [n][d] array.
 template <bool TILED>
@@ -45,11 +82,14 @@ __global__ __launch_bounds__(256) void k_export_rows(const uint16_t* __restrict_
 hipError_t launch_normalise(const void* in, int dtype, int64_t rows, int64_t rows_pad, int d, int d_pad,
                             uint16_t* out, int64_t row0, bool tiled, hipStream_t s) {
     if (rows_pad <= 0) return hipSuccess;
-    const dim3 grid((unsigned)grid_blocks((rows_pad + 3) / 4)), block(256);
-    if (tiled)
-        k_normalise_rows<true><<<grid, block, 0, s>>>(in, dtype, rows, rows_pad, d, d_pad, out, row0);
-    else
-        k_normalise_rows<false><<<grid, block, 0, s>>>(in, dtype, rows, rows_pad, d, d_pad, out, row0);
+    if (tiled) {
+        const int64_t groups = ((row0 + rows_pad + 15) >> 4) - (row0 >> 4);
+        k_normalise_tiled<<<dim3((unsigned)grid_blocks(groups)), dim3(256), 0, s>>>(in, dtype, rows, rows_pad, d,
+                                                                                   d_pad, out, row0);
+    } else {
+        k_normalise_rows<false><<<dim3((unsigned)grid_blocks((rows_pad + 3) / 4)), dim3(256), 0, s>>>(
+            in, dtype, rows, rows_pad, d, d_pad, out, row0);
+    }
     return hipGetLastError();
 }
 
