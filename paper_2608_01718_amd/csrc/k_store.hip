@@ -10,21 +10,56 @@
 
 namespace lacache {
 
-// One wave per row (grid-stride over the rows).  Rows >= rows (up to rows_pad) are written as zeros, as are the
-// columns d .. d_pad-1.
-template <bool TILED>
+// The row-major layout (prefix embeddings), one wave per row (grid-stride over the rows).  Rows >= rows (up to
+// rows_pad) are written as zeros, as are the columns d .. d_pad-1.  NC > 0 (d_pad <= 512 NC): each lane keeps
+// its 8 NC columns of the row in registers, read once; the norm is summed in the order row_norm uses and
+// every element rounded by the same routine, so the stored bits are those of normalise_row.  NC = 0: any d,
+// through normalise_row (the row read twice).
+template <int NC>
 __global__ __launch_bounds__(256) void k_normalise_rows(const void* __restrict__ in, int dtype, int64_t rows,
                                                         int64_t rows_pad, int d, int d_pad,
                                                         uint16_t* __restrict__ out, int64_t row0) {
     const int lane = threadIdx.x & 63;
-    const int kc = d_pad >> 5;
     for (int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); r < rows_pad; r += (int64_t)gridDim.x * 4) {
         const bool live = r < rows;
         const char* src = (const char*)in + (live ? r * (int64_t)d * (dtype == 0 ? 4 : 2) : 0);
-        normalise_row(src, dtype, d, d_pad, live, lane, [&](int j0, u32x4 w) {
-            const int64_t off = TILED ? tiled_offset(row0 + r, j0, kc) : (row0 + r) * (int64_t)d_pad + j0;
-            *(u32x4*)(out + off) = w;
-        });
+        uint16_t* dst = out + (row0 + r) * (int64_t)d_pad;
+        if constexpr (NC > 0) {
+            float x[NC][8];
+#pragma unroll
+            for (int c = 0; c < NC; ++c) {
+                if (live) {
+                    load8f(src, dtype, d, lane * 8 + 512 * c, x[c]);
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) x[c][e] = 0.0f;
+                }
+            }
+            double ss = 0.0;
+#pragma unroll
+            for (int c = 0; c < NC; ++c)
+#pragma unroll
+                for (int e = 0; e < 8; ++e) ss += (double)x[c][e] * (double)x[c][e];
+            const double n = __builtin_sqrt(wave_sum_f64(ss));
+            const double rn = 1.0 / n;
+#pragma unroll
+            for (int c = 0; c < NC; ++c) {
+                const int j0 = lane * 8 + 512 * c;
+                if (j0 >= d_pad) continue;
+                uint32_t h[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    h[e] = (live && j0 + e < d && n != 0.0) ? bf16_rne_quotient(x[c][e], n, rn) : 0u;
+                u32x4 w;
+                w.x = h[0] | (h[1] << 16);
+                w.y = h[2] | (h[3] << 16);
+                w.z = h[4] | (h[5] << 16);
+                w.w = h[6] | (h[7] << 16);
+                *(u32x4*)(dst + j0) = w;
+            }
+        } else {
+            normalise_row(src, dtype, d, d_pad, live, lane, [&](int j0, u32x4 w) { *(u32x4*)(dst + j0) = w; });
+        }
     }
 }
 
@@ -87,8 +122,15 @@ hipError_t launch_normalise(const void* in, int dtype, int64_t rows, int64_t row
         k_normalise_tiled<<<dim3((unsigned)grid_blocks(groups)), dim3(256), 0, s>>>(in, dtype, rows, rows_pad, d,
                                                                                    d_pad, out, row0);
     } else {
-        k_normalise_rows<false><<<dim3((unsigned)grid_blocks((rows_pad + 3) / 4)), dim3(256), 0, s>>>(
-            in, dtype, rows, rows_pad, d, d_pad, out, row0);
+        const dim3 grid((unsigned)grid_blocks((rows_pad + 3) / 4)), block(256);
+        if (d_pad <= 512)
+            k_normalise_rows<1><<<grid, block, 0, s>>>(in, dtype, rows, rows_pad, d, d_pad, out, row0);
+        else if (d_pad <= 1024)
+            k_normalise_rows<2><<<grid, block, 0, s>>>(in, dtype, rows, rows_pad, d, d_pad, out, row0);
+        else if (d_pad <= 2048)
+            k_normalise_rows<4><<<grid, block, 0, s>>>(in, dtype, rows, rows_pad, d, d_pad, out, row0);
+        else
+            k_normalise_rows<0><<<grid, block, 0, s>>>(in, dtype, rows, rows_pad, d, d_pad, out, row0);
     }
     return hipGetLastError();
 }
