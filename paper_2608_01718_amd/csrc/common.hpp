@@ -57,39 +57,53 @@ __host__ __device__ inline uint16_t bf16_rne_from_f64(double v) {
     return (uint16_t)(sign | (uint16_t)s);
 }
 
-// bfloat16 rounding of the quotient v / n, identical to bf16_rne_from_f64(v / n) with the division correctly
-// rounded, from q' = v * rn where rn = 1 / n correctly rounded.  q' is within 3 units in the last place of a
-// double of the rounded quotient q.  q' is rounded once more, to float32, and that to bfloat16.  Every
-// bfloat16 rounding midpoint is a float32, so the float32 lies on the same side of each midpoint as q' unless
-// it is that midpoint (its low 16 bits are 0x8000), and a midpoint between q' and q, 3 double units away at
-// most, would make the float32 that midpoint too.  So the result is exact unless the float32 is a midpoint;
-// those rare cases, zero and values below 2^-125 (where bfloat16 loses precision) divide.
-// The rounding without the division: the result as the float32 of the same value (its low 16 bits zero),
-// and whether it may be wrong (the float32 is a midpoint, zero, or below 2^-125), when the caller must take
-// bf16_rne_quotient_f32 instead.
-__host__ __device__ inline float bf16_rne_quotient_fast(double v, double rn, bool& exact_needed) {
-    const float f = (float)(v * rn);
+// bfloat16 rounding of the quotient v / n of a float32 v, identical to bf16_rne_from_f64(v / n) with the
+// division correctly rounded (call that double q), computed as f = v * rnf in float32, where rnf is 1 / n
+// rounded to double and then to float32 (quotient_rcp_f32).  The roundings of rn, rnf, f and q (at most
+// 2^-53, 2^-24, 2^-24 and 2^-53 relative) put f within 2^-23 (1 + 2^-28) |v / n| of q: at most 2 float32 units
+// in the last place of f's binade, plus a sliver.  Every bfloat16 rounding midpoint is a float32 with low 16
+// bits 0x8000, and the only one closer to f than 2^14 such units is the one inside f's own bfloat16 interval;
+// so unless f's low 16 bits are within 2 of 0x8000, no midpoint lies between f and q and both round to the
+// same bfloat16.  The fallback window is twice that (within 4).  Those rare cases, zero,
+// values below 2^-125 (where the float32 product loses relative precision) and rows whose reciprocal is not
+// a normal float32 (rnf = 0, so every product is zero) divide instead.
+// The reciprocal for bf16_rne_quotient_fast: 1 / n rounded to double, then to float32, or 0 where that double
+// is not a normal float32.
+__host__ __device__ inline float quotient_rcp_f32(double n) {
+    const double rn = 1.0 / n;
+    return (rn >= 0x1p-126 && rn < 0x1p127) ? (float)rn : 0.0f;
+}
+
+// The rounding without the division: the result as the float32 of the same value (its low 16 bits zero), and
+// whether it may be wrong, when the caller must take bf16_rne_quotient_f32 instead.
+__host__ __device__ inline float bf16_rne_quotient_fast(float v, float rnf, bool& exact_needed) {
+    const float f = v * rnf;
     uint32_t u;
     __builtin_memcpy(&u, &f, 4);
-    exact_needed = (u & 0x7FFFFFFFu) < 0x01000000u || (u & 0xFFFFu) == 0x8000u;
+    exact_needed = (u & 0x7FFFFFFFu) < 0x01000000u || (u & 0xFFFFu) - 0x7FFCu <= 8u;
     u = (u + 0x7FFFu + ((u >> 16) & 1u)) & 0xFFFF0000u;
     float r;
     __builtin_memcpy(&r, &u, 4);
     return r;
 }
 
-// The result as the float32 of the same value (its low 16 bits zero).
-__host__ __device__ inline float bf16_rne_quotient_f32(double v, double n, double rn) {
+// The result as the float32 of the same value (its low 16 bits zero); rnf = quotient_rcp_f32(n).
+__host__ __device__ inline float bf16_rne_quotient_f32(float v, double n, float rnf) {
     bool exact_needed;
-    const float r = bf16_rne_quotient_fast(v, rn, exact_needed);
+    const float r = bf16_rne_quotient_fast(v, rnf, exact_needed);
     if (!exact_needed) return r;
-    const uint32_t u = (uint32_t)bf16_rne_from_f64(v / n) << 16;
+    float vv = v;
+#if defined(__HIP_DEVICE_COMPILE__)
+    // convert here, on the rare path, rather than keep a double of every element live across the caller's loop
+    __asm__ volatile("" : "+v"(vv));
+#endif
+    const uint32_t u = (uint32_t)bf16_rne_from_f64((double)vv / n) << 16;
     float e;
     __builtin_memcpy(&e, &u, 4);
     return e;
 }
-__host__ __device__ inline uint16_t bf16_rne_quotient(double v, double n, double rn) {
-    const float r = bf16_rne_quotient_f32(v, n, rn);
+__host__ __device__ inline uint16_t bf16_rne_quotient(float v, double n, float rnf) {
+    const float r = bf16_rne_quotient_f32(v, n, rnf);
     uint32_t u;
     __builtin_memcpy(&u, &r, 4);
     return (uint16_t)(u >> 16);
@@ -187,14 +201,14 @@ __device__ inline double row_norm(const void* row, int dtype, int d, bool live, 
 // Columns j0 .. j0+7 of the normalised row as packed bfloat16 (zeros beyond d, for a zero norm or dead rows).
 __device__ inline u32x4 quantise8(const void* row, int dtype, int d, int j0, double n, bool live) {
     uint16_t h[8];
-    double v[8];
-    if (live && j0 < d && n != 0.0) load8(row, dtype, d, j0, v);
-    const double rn = 1.0 / n;
+    float v[8];
+    if (live && j0 < d && n != 0.0) load8f(row, dtype, d, j0, v);
+    const float rnf = quotient_rcp_f32(n);
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
         const int j = j0 + e;
         h[e] = 0;
-        if (live && j < d && n != 0.0) h[e] = bf16_rne_quotient(v[e], n, rn);
+        if (live && j < d && n != 0.0) h[e] = bf16_rne_quotient(v[e], n, rnf);
     }
     u32x4 w;
     w.x = (uint32_t)h[0] | ((uint32_t)h[1] << 16);

@@ -56,7 +56,7 @@ __device__ __forceinline__ void pair_cosine(const void* __restrict__ a, const vo
             }
         const double na = __builtin_sqrt(wave_sum_f64(sa)), nb = __builtin_sqrt(wave_sum_f64(sb));
         if (na != 0.0 && nb != 0.0) {  // a zero vector normalises to zero and scores 0
-            const double rna = 1.0 / na, rnb = 1.0 / nb;
+            const float rna = quotient_rcp_f32(na), rnb = quotient_rcp_f32(nb);
 #pragma unroll
             for (int c = 0; c < NC; ++c)
 #pragma unroll
@@ -69,11 +69,11 @@ __device__ __forceinline__ void pair_cosine(const void* __restrict__ a, const vo
         const double na = row_norm(ra, dtype, d, true, lane);
         const double nb = row_norm(rb, dtype, d, true, lane);
         if (na != 0.0 && nb != 0.0) {
-            const double rna = 1.0 / na, rnb = 1.0 / nb;
+            const float rna = quotient_rcp_f32(na), rnb = quotient_rcp_f32(nb);
             for (int j0 = lane * 8; j0 < d; j0 += 512) {
-                double va[8], vb[8];
-                load8(ra, dtype, d, j0, va);
-                load8(rb, dtype, d, j0, vb);
+                float va[8], vb[8];
+                load8f(ra, dtype, d, j0, va);
+                load8f(rb, dtype, d, j0, vb);
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
                     if (j0 + e >= d) continue;

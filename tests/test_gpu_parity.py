@@ -63,6 +63,39 @@ def test_store_matches_oracle_quantisation(lc):
         c.close()
 
 
+@pytest.mark.parametrize("d", [64, 384, 512, 520, 768, 1000, 1152, 2048, 2100])
+@pytest.mark.parametrize("dtype", [oracle.F32, oracle.BF16])
+def test_keys_and_prefix_rows_store_identically(lc, d, dtype):
+    """The same vectors inserted as keys (tiled layout: a norm pass, then a rounding pass) and as prefix
+    embeddings (row-major layout: each row held in registers up to d = 2048, two passes beyond) are stored
+    bit-identically: the normalisers sum the norm in one order and round every element alike.  Inserts in chunks of 777 rows, so groups of 16
+    rows straddle calls; among the rows, zero vectors, vectors of subnormal float32 components and vectors
+    near the top of the float32 range (their reciprocal norms are no normal float32); against the oracle's
+    quantisation as the store test checks it."""
+    rng = np.random.default_rng(1000 + d)
+    N = 1000
+    x = rng.standard_normal((N, d)).astype(np.float32)
+    x[5] = 0.0
+    x[17] *= np.float32(1e-41)
+    x[300] *= np.float32(2e37)
+    x[301] *= np.float32(1e-30)
+    src = x if dtype == oracle.F32 else (x.view(np.uint32) >> 16).astype(np.uint16)
+    tok = rng.integers(0, 1000, (N, 4), dtype=np.int32)
+    say(f"[case] keys vs prefix rows, d={d} dtype={dtype}")
+    c = lc.LaCache(N, d, 4, dtype, 16, 0)
+    for r0 in range(0, N, 777):
+        assert c.insert(to_dev(src[r0:r0 + 777]), to_dev(src[r0:r0 + 777]), to_dev(tok[r0:r0 + 777])) == r0
+    k, e, _ = (t.cpu().numpy() for t in c.export(0, N))
+    c.close()
+    np.testing.assert_array_equal(k.view(np.uint16), e.view(np.uint16))
+    want = oracle.quantise(src, dtype)
+    got = k.view(np.uint16)
+    diff = got != want
+    assert diff.mean() <= 1e-3
+    assert np.all(np.abs(got.astype(np.int32) - want.astype(np.int32))[diff] <= 1)
+    assert not got[5].any()
+
+
 def test_single_insert_and_export_beyond_one_grid(lc):
     """One insert of 4.3M rows (more rows than one launch of the normaliser covers: its waves loop) and one
     export of all of them (4.3M x 80 values, more than one launch of the export covers: its threads loop),
