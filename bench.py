@@ -157,20 +157,27 @@ def log(*a):
 
 def sclk_under_load(torch, step, seconds=1.5):
     """The GPU's shader clock (MHz) while `step` runs back to back: rocm-smi is sampled once, from a separate
-    thread, half a second into ~`seconds` of continuous calls.  None when the tool or its reading is missing."""
+    thread, half a second into ~`seconds` of continuous calls.  None when the tool or its reading is missing,
+    and under a profiler: its preloaded library would start up, and initialise the GPU, in the sampling
+    process too."""
     import re
     import shutil
     import subprocess
     import threading
+    if os.environ.get("ROCPROFILER_LIBRARY_CTOR") or "rocprofiler" in os.environ.get("LD_PRELOAD", ""):
+        return None
     smi = shutil.which("rocm-smi")
     if smi is None:
         return None
+    # the tool is a Python script: run it with this interpreter rather than through its `env` line
+    smi = os.path.realpath(smi)
+    cmd = [sys.executable, smi] if smi.endswith(".py") else [smi]
     got = {}
 
     def sample():
         time.sleep(0.5)
         try:
-            r = subprocess.run([smi, "--showclocks", "--json"], capture_output=True, text=True, timeout=20)
+            r = subprocess.run(cmd + ["--showclocks", "--json"], capture_output=True, text=True, timeout=20)
             m = re.search(r"sclk clock speed:\"\s*:\s*\"\((\d+)Mhz\)", r.stdout)
             got["mhz"] = int(m.group(1)) if m else None
         except (OSError, subprocess.SubprocessError):

@@ -63,17 +63,18 @@ def test_store_matches_oracle_quantisation(lc):
         c.close()
 
 
+@pytest.mark.parametrize("N,chunk", [(1000, 777), (9000, 9000)])
 @pytest.mark.parametrize("d", [64, 384, 512, 520, 768, 1000, 1152, 2048, 2100])
 @pytest.mark.parametrize("dtype", [oracle.F32, oracle.BF16])
-def test_keys_and_prefix_rows_store_identically(lc, d, dtype):
-    """The same vectors inserted as keys (tiled layout: a norm pass, then a rounding pass) and as prefix
-    embeddings (row-major layout: each row held in registers up to d = 2048, two passes beyond) are stored
-    bit-identically: the normalisers sum the norm in one order and round every element alike.  Inserts in chunks of 777 rows, so groups of 16
-    rows straddle calls; among the rows, zero vectors, vectors of subnormal float32 components and vectors
-    near the top of the float32 range (their reciprocal norms are no normal float32); against the oracle's
-    quantisation as the store test checks it."""
+def test_keys_and_prefix_rows_store_identically(lc, N, chunk, d, dtype):
+    """The same vectors inserted as keys (tiled layout) and as prefix embeddings (row-major layout) are stored
+    bit-identically: every normaliser sums the norm in one order and rounds every element alike.  Keys of
+    calls up to 8192 rows take a wave per row (rows held in registers up to d = 2048), larger calls a norm
+    pass and a rounding pass; prefix rows are held in registers up to d = 2048, two passes beyond.  Inserts
+    in chunks of 777 rows (groups of 16 rows straddle calls) or one insert of 9000; among the rows, zero
+    vectors, vectors of subnormal float32 components and vectors near the top of the float32 range (their
+    reciprocal norms are no normal float32); against the oracle's quantisation as the store test checks it."""
     rng = np.random.default_rng(1000 + d)
-    N = 1000
     x = rng.standard_normal((N, d)).astype(np.float32)
     x[5] = 0.0
     x[17] *= np.float32(1e-41)
@@ -81,10 +82,10 @@ def test_keys_and_prefix_rows_store_identically(lc, d, dtype):
     x[301] *= np.float32(1e-30)
     src = x if dtype == oracle.F32 else (x.view(np.uint32) >> 16).astype(np.uint16)
     tok = rng.integers(0, 1000, (N, 4), dtype=np.int32)
-    say(f"[case] keys vs prefix rows, d={d} dtype={dtype}")
+    say(f"[case] keys vs prefix rows, N={N} chunk={chunk} d={d} dtype={dtype}")
     c = lc.LaCache(N, d, 4, dtype, 16, 0)
-    for r0 in range(0, N, 777):
-        assert c.insert(to_dev(src[r0:r0 + 777]), to_dev(src[r0:r0 + 777]), to_dev(tok[r0:r0 + 777])) == r0
+    for r0 in range(0, N, chunk):
+        assert c.insert(to_dev(src[r0:r0 + chunk]), to_dev(src[r0:r0 + chunk]), to_dev(tok[r0:r0 + chunk])) == r0
     k, e, _ = (t.cpu().numpy() for t in c.export(0, N))
     c.close()
     np.testing.assert_array_equal(k.view(np.uint16), e.view(np.uint16))
