@@ -27,10 +27,11 @@
 // tile, so ties keep the lowest group.  The exact lowest row is recovered
 // afterwards by replaying the winning group (verify.hpp), which keeps this
 // epilogue branch-free.  The one partial key tile (rows beyond the entry
-// count are zero padding and must not win) is handled by a separate, masked
-// instantiation (a masked epilogue inside the main loop measured 3 % slower:
-// it adds scalar-register pressure to every stage).  At the end each
-// workgroup writes one packed candidate per query.
+// count are zero padding and must not win) is handled by separate, masked
+// workgroups of the same launch, dispatched first so that they overlap the
+// full tiles (a masked epilogue inside the main loop measured 3 % slower: it
+// adds scalar-register pressure to every stage).  At the end each workgroup
+// writes one packed candidate per query.
 #include <type_traits>
 
 #include "common.hpp"
@@ -76,36 +77,17 @@ __device__ inline void buffer_to_lds16(__amdgpu_buffer_rsrc_t r, uint32_t voff, 
 
 }  // namespace
 
-// MASKED = false: key tiles [0, n_ktiles) are all full; they are split into n_ranges contiguous ranges and
-// range r writes partial slot r.  MASKED = true: the single partial tile n_ktiles (rows n_ktiles*256 ..
-// n_rows-1), written to partial slot `slot`.  P is the partial stride of a query.  xq selects the XCD
-// placement of the workgroups (below); it requires n_qtiles % xq == 0 and n_ranges % (8 / xq) == 0.
+// One workgroup's work: query tile qtile against key tiles [kt0, kt1), its candidates written to partial
+// slot `slot` (P is the partial stride of a query).  MASKED = false: every tile is full.  MASKED = true: the
+// single partial tile (rows beyond n_rows are zero padding and must not win).
 template <bool MASKED>
-__global__ __launch_bounds__(512, 1) void k_stage1_gemm(const u32x4* __restrict__ keys, const u32x4* __restrict__ qt,
-                                                        int kc, int n_rows, int B, int n_qtiles, int n_ktiles,
-                                                        int n_ranges, int slot, int P, int xq,
-                                                        uint64_t* __restrict__ part) {
+__device__ __forceinline__ void gemm_tiles(const u32x4* __restrict__ keys, const u32x4* __restrict__ qt, int kc,
+                                           int n_rows, int B, int qtile, int kt0, int kt1, int slot, int P,
+                                           uint64_t* __restrict__ part) {
     extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
     const int tid = threadIdx.x, lane = tid & 63;
     const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform, kept in scalar registers
     const int wk = wid & 1, wq = wid >> 1;                     // key half (128 keys), query quarter (64)
-
-    // workgroup -> (query tile, key range).  Dispatch is round-robin over the 8 XCDs (one L2 each).  With
-    // xq > 0 the XCDs form xq query groups x (8 / xq) key parts: XCD x serves the query tiles of group
-    // x % xq (small enough to stay in its L2) against key part x / xq, and consecutive workgroups of an XCD
-    // take consecutive query tiles of one key range, so that range's keys come into that L2 once.
-    int qtile, range;
-    if (xq > 0) {
-        const int xcd = blockIdx.x % 8, j = blockIdx.x / 8;
-        const int qpg = n_qtiles / xq, rpp = n_ranges / (8 / xq);
-        qtile = (xcd % xq) * qpg + j % qpg;
-        range = (xcd / xq) * rpp + j / qpg;
-    } else {
-        qtile = blockIdx.x % n_qtiles;
-        range = blockIdx.x / n_qtiles;
-    }
-    const int kt0 = MASKED ? n_ktiles : (int)((int64_t)range * n_ktiles / n_ranges);
-    const int kt1 = MASKED ? n_ktiles + 1 : (int)((int64_t)(range + 1) * n_ktiles / n_ranges);
     const int spt = kc / kBlk;                // stages per key tile
     const int T = (kt1 - kt0) * spt;          // stages of the whole range
 
@@ -262,8 +244,50 @@ __global__ __launch_bounds__(512, 1) void k_stage1_gemm(const u32x4* __restrict_
     if (tid < kTile) {
         const uint64_t m = umax64(red[tid], red[kTile + tid]);
         const int gq = qtile * kTile + tid;
-        if (gq < B) part[(int64_t)gq * P + (MASKED ? slot : range)] = m;
+        if (gq < B) part[(int64_t)gq * P + slot] = m;
     }
+}
+
+// The partial key tile n_ktiles for query tile qtile, into partial slot P - 1.  Kept out of line: its masked
+// epilogue needs more scalar registers than the hardware has (the spills stay in this function), and inlined
+// into the kernel it would take the full tiles' loop down with it.
+__device__ __attribute__((noinline)) void gemm_tail(const u32x4* __restrict__ keys, const u32x4* __restrict__ qt,
+                                                    int kc, int n_rows, int B, int qtile, int n_ktiles, int P,
+                                                    uint64_t* __restrict__ part) {
+    gemm_tiles<true>(keys, qt, kc, n_rows, B, qtile, n_ktiles, n_ktiles + 1, P - 1, P, part);
+}
+
+// The first tail_blocks workgroups (n_qtiles of them, padded to a multiple of 8 so that the others keep their
+// XCD) take the single partial key tile n_ktiles, one query tile each, into partial slot P - 1; they are
+// dispatched first and overlap the full tiles.  The other workgroups split the full key tiles [0, n_ktiles)
+// into n_ranges contiguous ranges, range r into partial slot r.  xq selects the XCD placement of those
+// (below); it requires n_qtiles % xq == 0 and n_ranges % (8 / xq) == 0.
+__global__ __launch_bounds__(512, 1) void k_stage1_gemm(const u32x4* __restrict__ keys, const u32x4* __restrict__ qt,
+                                                        int kc, int n_rows, int B, int n_qtiles, int n_ktiles,
+                                                        int n_ranges, int tail_blocks, int P, int xq,
+                                                        uint64_t* __restrict__ part) {
+    if ((int)blockIdx.x < tail_blocks) {
+        if ((int)blockIdx.x < n_qtiles) gemm_tail(keys, qt, kc, n_rows, B, blockIdx.x, n_ktiles, P, part);
+        return;
+    }
+    const int bid = (int)blockIdx.x - tail_blocks;
+    // workgroup -> (query tile, key range).  Dispatch is round-robin over the 8 XCDs (one L2 each).  With
+    // xq > 0 the XCDs form xq query groups x (8 / xq) key parts: XCD x serves the query tiles of group
+    // x % xq (small enough to stay in its L2) against key part x / xq, and consecutive workgroups of an XCD
+    // take consecutive query tiles of one key range, so that range's keys come into that L2 once.
+    int qtile, range;
+    if (xq > 0) {
+        const int xcd = bid % 8, j = bid / 8;
+        const int qpg = n_qtiles / xq, rpp = n_ranges / (8 / xq);
+        qtile = (xcd % xq) * qpg + j % qpg;
+        range = (xcd / xq) * rpp + j / qpg;
+    } else {
+        qtile = bid % n_qtiles;
+        range = bid / n_qtiles;
+    }
+    const int kt0 = (int)((int64_t)range * n_ktiles / n_ranges);
+    const int kt1 = (int)((int64_t)(range + 1) * n_ktiles / n_ranges);
+    gemm_tiles<false>(keys, qt, kc, n_rows, B, qtile, kt0, kt1, range, P, part);
 }
 
 hipError_t launch_stage1_gemm(const uint16_t* keys, const uint16_t* qt, int B, int n_rows, int d_pad, uint64_t* part,
@@ -293,16 +317,13 @@ hipError_t launch_stage1_gemm(const uint16_t* keys, const uint16_t* qt, int B, i
         }
     }
     const size_t lds = (size_t)kNBuf * kStageBytes;
-    static std::atomic<uint64_t> lds_full{0}, lds_tail{0};
-    hipError_t e = allow_dynamic_lds((const void*)k_stage1_gemm<false>, (int)lds, lds_full);
-    if (e == hipSuccess) e = allow_dynamic_lds((const void*)k_stage1_gemm<true>, (int)lds, lds_tail);
+    static std::atomic<uint64_t> lds_done{0};
+    hipError_t e = allow_dynamic_lds((const void*)k_stage1_gemm, (int)lds, lds_done);
     if (e != hipSuccess) return e;
-    if (n_ranges > 0)
-        k_stage1_gemm<false><<<dim3(grid), dim3(kWaves * 64), lds, s>>>(
-            (const u32x4*)keys, (const u32x4*)qt, kc, n_rows, B, n_qtiles, n_full, n_ranges, 0, P, xq, part);
-    if (tail)
-        k_stage1_gemm<true><<<dim3(n_qtiles), dim3(kWaves * 64), lds, s>>>(
-            (const u32x4*)keys, (const u32x4*)qt, kc, n_rows, B, n_qtiles, n_full, 1, P - 1, P, 0, part);
+    // the partial tile's workgroups first (a separate launch after the full tiles measured 23 us on its own)
+    const int tail_blocks = tail ? (n_qtiles + 7) / 8 * 8 : 0;
+    k_stage1_gemm<<<dim3(tail_blocks + grid), dim3(kWaves * 64), lds, s>>>(
+        (const u32x4*)keys, (const u32x4*)qt, kc, n_rows, B, n_qtiles, n_full, n_ranges, tail_blocks, P, xq, part);
     return hipGetLastError();
 }
 

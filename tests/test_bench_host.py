@@ -39,7 +39,7 @@ def test_pmc_summary_scales_by_the_copy(tmp_path):
               [("copy_kernel", copy_mib * 1024 / 2)])
     _counters(str(root / "write_copy" / "run_counter_collection.csv"), "WRITE_SIZE",
               [("copy_kernel", copy_mib * 1024)])
-    gemm, stream = "void lacache::k_stage1_gemm<false>(...)", "void lacache::k_stage1_stream<1, true>(...)"
+    gemm, stream = "lacache::k_stage1_gemm(...)", "void lacache::k_stage1_stream<1, true>(...)"
     _counters(str(root / "fetch_bench" / "run_counter_collection.csv"), "FETCH_SIZE",
               [(gemm, 3.0e6), (gemm, 3.2e6), (gemm, 9.9e9), (stream, 750_000.0), (stream, 750_001.0),
                (stream, 10.0), ("other", 1.0)])

@@ -4,6 +4,7 @@ test_oracle_pins.py fail, while the unmodified source passes the same pipeline."
 import os
 import subprocess
 import sys
+from concurrent.futures import ThreadPoolExecutor
 
 import pytest
 
@@ -58,26 +59,52 @@ MUTANTS = {
 }
 
 
-def _run_pins(tmp_path, source: str, tag: str) -> int:
+WORKERS = max(1, min(8, os.cpu_count() or 1))
+
+
+def _run_pins(tmp_path, source: str, tag: str, threads: int) -> int:
     c = tmp_path / f"{tag}.c"
     so = tmp_path / f"{tag}.so"
     c.write_text(source)
     subprocess.run(["gcc", "-O2", "-fopenmp", "-std=c11", "-shared", "-fPIC", "-o", str(so), str(c), "-lm"],
                    check=True)
-    env = dict(os.environ, LACACHE_ORACLE_LIB=str(so))
+    env = dict(os.environ, LACACHE_ORACLE_LIB=str(so), OMP_NUM_THREADS=str(threads))
     r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
                         os.path.join(ROOT, "tests", "test_oracle_pins.py")], cwd=ROOT, env=env,
                        capture_output=True, text=True)
     return r.returncode
 
 
-def test_unmodified_source_passes_the_pins(tmp_path):
-    assert _run_pins(tmp_path, open(SRC).read(), "original") == 0
+@pytest.fixture(scope="module")
+def pin_runs(tmp_path_factory):
+    """Exit status of the pin suite on the unmodified source and on every mutant, run side by side (one
+    process per source, the host's cores shared among them)."""
+    src = open(SRC).read()
+    jobs = {"": src}
+    for i, (name, (old, new)) in enumerate(sorted(MUTANTS.items())):
+        if src.count(old) == 1:
+            jobs[name] = src.replace(old, new)
+    threads = max(1, (os.cpu_count() or 1) // WORKERS)
+    base = tmp_path_factory.mktemp("mutants")
+    dirs = {name: base / f"m{i}" for i, name in enumerate(jobs)}
+    for p in dirs.values():
+        p.mkdir()
+
+    def run(name):
+        return name, _run_pins(dirs[name], jobs[name], "oracle", threads)
+
+    with ThreadPoolExecutor(WORKERS) as pool:
+        return dict(pool.map(run, jobs))
+
+
+def test_unmodified_source_passes_the_pins(pin_runs):
+    assert pin_runs[""] == 0
 
 
 @pytest.mark.parametrize("name", sorted(MUTANTS))
-def test_planted_mistake_is_caught(tmp_path, name):
+def test_planted_mistake_is_caught(pin_runs, name):
     old, new = MUTANTS[name]
     src = open(SRC).read()
     assert src.count(old) == 1, f"mutation anchor not found (or ambiguous): {name}"
-    assert _run_pins(tmp_path, src.replace(old, new), "mutant") != 0, f"pins did not catch: {name}"
+    # pytest's status 1: the suite ran and a pin failed (not a crash, a usage error or an interruption)
+    assert pin_runs[name] == 1, f"pins did not catch: {name} (status {pin_runs[name]})"
