@@ -20,7 +20,10 @@ namespace lacache {
 // Exact row of query b inside the 32-row group g that the GEMM path reported: replay the group against
 // the same 32-query fragment with the same MFMA sequence (v_mfma_f32_32x32x16_bf16 over the 16-column
 // steps in order, from a zero accumulator), which reproduces the GEMM's float32 scores bit for bit, and
-// take the lowest stored row whose score equals s.  Returns -1 if none does.
+// take the lowest stored row whose score equals s.  Returns -1 if none does.  The operand fragments are
+// loaded kReplayBatch steps at a time, so the chain of MFMAs waits for memory 2 kc / kReplayBatch times
+// rather than once per step.
+constexpr int kReplayBatch = 16;
 __device__ inline int32_t replay_group(const u32x4* __restrict__ keys, const u32x4* __restrict__ qt, int kc, int b, int g,
                                 float s, int n_rows, int lane) {
     const int kr = g * 32 + (lane & 31);       // key row this lane feeds (row operand)
@@ -28,9 +31,21 @@ __device__ inline int32_t replay_group(const u32x4* __restrict__ keys, const u32
     const u32x4* kp = keys + (int64_t)(kr >> 4) * kc * 64 + (kr & 15);
     const u32x4* qp = qt + (int64_t)(qr >> 4) * kc * 64 + (qr & 15);
     f32x16 acc = f32x16{};
-    for (int st = 0; st < 2 * kc; ++st) {
-        const int off = (st >> 1) * 64 + (((st & 1) << 1) + (lane >> 5)) * 16;
-        acc = mfma32x32x16(kp[off], qp[off], st == 0 ? f32x16{} : acc);
+    const int n = 2 * kc;
+    for (int st0 = 0; st0 < n; st0 += kReplayBatch) {
+        u32x4 ka[kReplayBatch], qa[kReplayBatch];
+#pragma unroll
+        for (int u = 0; u < kReplayBatch; ++u) {
+            const int st = st0 + u;
+            if (st < n) {
+                const int off = (st >> 1) * 64 + (((st & 1) << 1) + (lane >> 5)) * 16;
+                ka[u] = kp[off];
+                qa[u] = qp[off];
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kReplayBatch; ++u)
+            if (st0 + u < n) acc = mfma32x32x16(ka[u], qa[u], acc);
     }
     int row = 0x7FFFFFFF;
     if ((lane & 31) == (b & 31)) {
