@@ -224,6 +224,46 @@ __device__ inline void normalise_row(const void* row, int dtype, int d, int d_pa
     for (int j0 = lane * 8; j0 < d_pad; j0 += 512) emit(j0, quantise8(row, dtype, d, j0, n, live));
 }
 
+// A row held in registers: lane l keeps columns l*8 + 512 c .. +7 for c < NC (zeros beyond d, and for rows that
+// are not live), the columns row_norm and quantise8 give lane l.
+template <int NC>
+__device__ __forceinline__ void row_to_regs(const char* src, int dtype, int d, bool live, int lane, float (&x)[NC][8]) {
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+        if (live) {
+            load8f(src, dtype, d, lane * 8 + 512 * c, x[c]);
+        } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) x[c][e] = 0.0f;
+        }
+    }
+}
+
+// Its norm, the squares summed in the order row_norm uses (the zeros it skips add nothing), so the two agree
+// bit for bit.
+template <int NC>
+__device__ __forceinline__ double regs_norm(const float (&x)[NC][8]) {
+    double ss = 0.0;
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) ss += (double)x[c][e] * (double)x[c][e];
+    return __builtin_sqrt(wave_sum_f64(ss));
+}
+
+// Columns j0 .. j0+7 of the row in registers (x = its c-th piece) rounded as quantise8 rounds them.
+__device__ __forceinline__ u32x4 regs_quantise8(const float (&x)[8], int j0, int d, double n, float rnf, bool live) {
+    uint32_t h[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) h[e] = (live && j0 + e < d && n != 0.0) ? bf16_rne_quotient(x[e], n, rnf) : 0u;
+    u32x4 w;
+    w.x = h[0] | (h[1] << 16);
+    w.y = h[2] | (h[3] << 16);
+    w.z = h[4] | (h[5] << 16);
+    w.w = h[6] | (h[7] << 16);
+    return w;
+}
+
 // Dot product of two packed bfloat16 chunks, accumulated into acc in float32 in column order.  bf16 x bf16
 // products are exact in float.
 __device__ inline float dot8_bf16(u32x4 a, u32x4 b, float acc) {

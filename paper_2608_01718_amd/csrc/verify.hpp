@@ -21,9 +21,25 @@ namespace lacache {
 // the same 32-query fragment with the same MFMA sequence (v_mfma_f32_32x32x16_bf16 over the 16-column
 // steps in order, from a zero accumulator), which reproduces the GEMM's float32 scores bit for bit, and
 // take the lowest stored row whose score equals s.  Returns -1 if none does.  The operand fragments are
-// loaded kReplayBatch steps at a time, so the chain of MFMAs waits for memory 2 kc / kReplayBatch times
-// rather than once per step.
-constexpr int kReplayBatch = 16;
+// loaded 16 steps at a time (the 2 kc steps are a multiple of 8: full batches of 16, then at most one of 8),
+// each batch without branches, so the chain of MFMAs waits for memory about kc / 8 times rather than once per
+// step.
+template <int S>
+__device__ __forceinline__ void replay_batch(const u32x4* __restrict__ kp, const u32x4* __restrict__ qp, int st0,
+                                             int lane, f32x16& acc) {
+    u32x4 ka[S], qa[S];
+#pragma unroll
+    for (int u = 0; u < S; ++u) {
+        const int st = st0 + u;
+        const int off = (st >> 1) * 64 + (((st & 1) << 1) + (lane >> 5)) * 16;
+        ka[u] = kp[off];
+        qa[u] = qp[off];
+    }
+    __builtin_amdgcn_sched_barrier(0);  // every load of the batch issued before the first MFMA waits
+#pragma unroll
+    for (int u = 0; u < S; ++u) acc = mfma32x32x16(ka[u], qa[u], acc);
+}
+
 __device__ inline int32_t replay_group(const u32x4* __restrict__ keys, const u32x4* __restrict__ qt, int kc, int b, int g,
                                 float s, int n_rows, int lane) {
     const int kr = g * 32 + (lane & 31);       // key row this lane feeds (row operand)
@@ -32,21 +48,9 @@ __device__ inline int32_t replay_group(const u32x4* __restrict__ keys, const u32
     const u32x4* qp = qt + (int64_t)(qr >> 4) * kc * 64 + (qr & 15);
     f32x16 acc = f32x16{};
     const int n = 2 * kc;
-    for (int st0 = 0; st0 < n; st0 += kReplayBatch) {
-        u32x4 ka[kReplayBatch], qa[kReplayBatch];
-#pragma unroll
-        for (int u = 0; u < kReplayBatch; ++u) {
-            const int st = st0 + u;
-            if (st < n) {
-                const int off = (st >> 1) * 64 + (((st & 1) << 1) + (lane >> 5)) * 16;
-                ka[u] = kp[off];
-                qa[u] = qp[off];
-            }
-        }
-#pragma unroll
-        for (int u = 0; u < kReplayBatch; ++u)
-            if (st0 + u < n) acc = mfma32x32x16(ka[u], qa[u], acc);
-    }
+    int st0 = 0;
+    for (; st0 + 16 <= n; st0 += 16) replay_batch<16>(kp, qp, st0, lane, acc);
+    if (st0 < n) replay_batch<8>(kp, qp, st0, lane, acc);
     int row = 0x7FFFFFFF;
     if ((lane & 31) == (b & 31)) {
 #pragma unroll
@@ -80,18 +84,45 @@ __device__ inline void verify_query(int b, uint64_t m, int32_t i, float s_raw, i
         return;
     }
 
+    // the first 64 of the first k tokens (lane j: token j), loaded with the first model's rows below
+    const int32_t* ut = la_tok + (int64_t)b * k;
+    const int32_t* tt = tokens + (int64_t)i * k_cap;
+    const bool has0 = lane < k;
+    const int32_t u0 = has0 ? ut[lane] : 0, t0 = has0 ? tt[lane] : 0;
+
     // for every prefix model: normalise the lookahead embedding exactly as stored vectors are and dot it with
     // the entry's stored prefix row; the embedding check passes only if every model reaches its threshold
     // (Section 4.4: with m lookahead checks a hit needs all of them)
     const size_t esz = dtype == 0 ? 4 : 2;
     bool all_pass = true;
     for (int mi = 0; mi < M.m; ++mi) {
-        const char* src = (const char*)M.la[mi] + (int64_t)b * M.d[mi] * esz;
-        const u32x4* er = (const u32x4*)(M.emb[mi] + (int64_t)i * M.d_pad[mi]);
+        const int d = M.d[mi], d_pad = M.d_pad[mi];
+        const char* src = (const char*)M.la[mi] + (int64_t)b * d * esz;
+        const u32x4* er = (const u32x4*)(M.emb[mi] + (int64_t)i * d_pad);
         float acc = 0.0f;
         // padded columns are zero on both sides
-        normalise_row(src, dtype, M.d[mi], M.d_pad[mi], true, lane,
-                      [&](int j0, u32x4 w) { acc = dot8_bf16(w, er[j0 >> 3], acc); });
+        if (d_pad <= 1024) {
+            // both rows loaded at once, the lookahead row kept in registers: the same norm, rounding and
+            // dot order as normalise_row, one wait for memory instead of three
+            float x[2][8];
+            u32x4 e[2];
+#pragma unroll
+            for (int c = 0; c < 2; ++c) {
+                const int j0 = lane * 8 + 512 * c;
+                e[c] = j0 < d_pad ? er[j0 >> 3] : u32x4{0u, 0u, 0u, 0u};
+            }
+            row_to_regs<2>(src, dtype, d, true, lane, x);
+            const double n = regs_norm<2>(x);
+            const float rnf = quotient_rcp_f32(n);
+#pragma unroll
+            for (int c = 0; c < 2; ++c) {
+                const int j0 = lane * 8 + 512 * c;
+                if (j0 < d_pad) acc = dot8_bf16(regs_quantise8(x[c], j0, d, n, rnf, true), e[c], acc);
+            }
+        } else {
+            normalise_row(src, dtype, d, d_pad, true, lane,
+                          [&](int j0, u32x4 w) { acc = dot8_bf16(w, er[j0 >> 3], acc); });
+        }
         acc = wave_sum_f32(acc);
         const float r = fminf(fmaxf(acc, -1.0f), 1.0f);
         if (lane == 0) resp_out[(int64_t)b * M.m + mi] = r;
@@ -99,10 +130,8 @@ __device__ inline void verify_query(int b, uint64_t m, int32_t i, float s_raw, i
     }
 
     // first k tokens: lane j compares token j, 64 at a time
-    bool tok_eq = true;
-    const int32_t* ut = la_tok + (int64_t)b * k;
-    const int32_t* tt = tokens + (int64_t)i * k_cap;
-    for (int j0 = 0; j0 < k; j0 += kWave) {
+    bool tok_eq = __ballot(has0 && u0 != t0) == 0ull;
+    for (int j0 = kWave; j0 < k; j0 += kWave) {
         const int j = j0 + lane;
         const bool differ = (j < k) && (ut[j] != tt[j]);
         if (__ballot(differ) != 0ull) tok_eq = false;
