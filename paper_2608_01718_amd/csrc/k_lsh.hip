@@ -80,22 +80,64 @@ __global__ __launch_bounds__(256) void k_simhash(const u32x4* __restrict__ rows_
     }
 }
 
+// Signature word of 16 rounded queries against hyperplanes b0 (bits 0..15 of the word) and b1 (16..31): S
+// column chunks c0 .. c0+S-1, every operand load of the batch issued before its first MFMA.  xat(c) gives the
+// lane's piece of query chunk c.
+template <int S, class X>
+__device__ __forceinline__ void simhash_batch(X xat, const u32x4* __restrict__ b0, const u32x4* __restrict__ b1,
+                                              int c0, f32x4& lo, f32x4& hi) {
+    u32x4 x[S], y0[S], y1[S];
+#pragma unroll
+    for (int u = 0; u < S; ++u) {
+        x[u] = xat(c0 + u);
+        y0[u] = b0[(c0 + u) * 64];
+        y1[u] = b1[(c0 + u) * 64];
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int u = 0; u < S; ++u) {
+        lo = mfma16x16x32(x[u], y0[u], lo);
+        hi = mfma16x16x32(x[u], y1[u], hi);
+    }
+}
+
 // Query preparation for the LSH lookup, one workgroup of 16 waves per 16 queries: wave w normalises and
 // rounds query 16 g + w into the tiled scratch exactly as stored vectors are (zeros past the batch) and
 // clears its candidate count; after the barrier wave w < bits / 32 computes signature word w of the 16
-// queries as k_simhash does.
+// queries with the MFMA sequence of k_simhash (so a query equal to a stored key gets its signature).
+// NC > 0 (d_pad <= 512 NC): the query row is read once into registers, and the rounded queries are also
+// kept in LDS (the tiled chunk layout), where the signature MFMAs read them; the hyperplane chunks are
+// loaded eight at a time.  NC = 0: any d, the rows read twice and the queries read back from the scratch.
+template <int NC>
 __global__ __launch_bounds__(1024) void k_lsh_prep(const void* __restrict__ queries, int dtype, int nb, int d,
                                                    int d_pad, uint16_t* __restrict__ qt,
                                                    const u32x4* __restrict__ hp_tiled, int bits,
                                                    uint32_t* __restrict__ sigq, uint32_t* __restrict__ cnt) {
+    __shared__ u32x4 qs[NC > 0 ? 16 * 64 * NC : 1];
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
     const int g = blockIdx.x;
     const int r = g * 16 + wv;
     const bool live = r < nb;
     const int kc = d_pad >> 5;
     const char* src = (const char*)queries + (live ? (int64_t)r * d * (dtype == 0 ? 4 : 2) : 0);
-    normalise_row(src, dtype, d, d_pad, live, lane,
-                  [&](int j0, u32x4 w) { *(u32x4*)(qt + tiled_offset(r, j0, kc)) = w; });
+    if constexpr (NC > 0) {
+        float x[NC][8];
+        row_to_regs<NC>(src, dtype, d, live, lane, x);
+        const double n = regs_norm<NC>(x);
+        const float rnf = quotient_rcp_f32(n);
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            const int j0 = lane * 8 + 512 * c, J = j0 >> 3;
+            if (j0 < d_pad) {
+                const u32x4 w = regs_quantise8(x[c], j0, d, n, rnf, live);
+                *(u32x4*)(qt + tiled_offset(r, j0, kc)) = w;
+                qs[(J >> 2) * 64 + (J & 3) * 16 + wv] = w;
+            }
+        }
+    } else {
+        normalise_row(src, dtype, d, d_pad, live, lane,
+                      [&](int j0, u32x4 w) { *(u32x4*)(qt + tiled_offset(r, j0, kc)) = w; });
+    }
     if (live && lane == 0) cnt[r] = 0u;
     __syncthreads();
     const int words = bits >> 5;
@@ -104,20 +146,10 @@ __global__ __launch_bounds__(1024) void k_lsh_prep(const void* __restrict__ quer
     const u32x4* b0 = hp_tiled + (int64_t)(2 * wv) * kc * 64 + lane;
     const u32x4* b1 = b0 + (int64_t)kc * 64;
     f32x4 lo = f32x4{0.f, 0.f, 0.f, 0.f}, hi = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int c = 0; c < kc; c += 4) {
-        u32x4 x[4], y0[4], y1[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            x[u] = a[(c + u) * 64];
-            y0[u] = b0[(c + u) * 64];
-            y1[u] = b1[(c + u) * 64];
-        }
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            lo = mfma16x16x32(x[u], y0[u], lo);
-            hi = mfma16x16x32(x[u], y1[u], hi);
-        }
-    }
+    auto xat = [&](int c) { return NC > 0 ? qs[c * 64 + lane] : a[c * 64]; };
+    int c = 0;
+    for (; c + 8 <= kc; c += 8) simhash_batch<8>(xat, b0, b1, c, lo, hi);
+    if (c < kc) simhash_batch<4>(xat, b0, b1, c, lo, hi);  // kc is a multiple of 4
     uint32_t word = 0u;
 #pragma unroll
     for (int half = 0; half < 2; ++half) {
@@ -250,8 +282,16 @@ hipError_t launch_lsh_lookup(const void* queries, int dtype, int nb, int d, int 
     if (nb <= 0) return hipSuccess;
     const int words = bits >> 5;
     if (words < 1 || words > 8) return hipErrorInvalidValue;
-    k_lsh_prep<<<dim3((unsigned)((nb + 15) / 16)), dim3(1024), 0, s>>>(queries, dtype, nb, d, d_pad, qt,
-                                                                      (const u32x4*)hp_tiled, bits, sigq, cnt);
+    const dim3 pg((unsigned)((nb + 15) / 16)), pb(1024);
+    const u32x4* hp = (const u32x4*)hp_tiled;
+    if (d_pad <= 512)
+        k_lsh_prep<1><<<pg, pb, 0, s>>>(queries, dtype, nb, d, d_pad, qt, hp, bits, sigq, cnt);
+    else if (d_pad <= 1024)
+        k_lsh_prep<2><<<pg, pb, 0, s>>>(queries, dtype, nb, d, d_pad, qt, hp, bits, sigq, cnt);
+    else if (d_pad <= 2048)
+        k_lsh_prep<4><<<pg, pb, 0, s>>>(queries, dtype, nb, d, d_pad, qt, hp, bits, sigq, cnt);
+    else
+        k_lsh_prep<0><<<pg, pb, 0, s>>>(queries, dtype, nb, d, d_pad, qt, hp, bits, sigq, cnt);
     // every thread a whole run of kScanKeys entries (no idle slots), at most 8 workgroups per CU
     int64_t blocks = (n_rows + 256 * kScanKeys - 1) / (256 * kScanKeys);
     if (blocks > 8 * num_cu) blocks = 8 * num_cu;
