@@ -113,12 +113,16 @@ def _check_lookup(g, o, sk, pk, sq, pq, kq, qq, radius, sp):
     return exempt
 
 
-@pytest.mark.parametrize("name,N,bits,radius", [("tiny", 3000, 64, 12), ("mid", 20000, 256, 64),
-                                                ("mid_paper", 10000, 128, 30), ("serve_small", 30000, 256, 64)])
-def test_lsh_parity(lc, name, N, bits, radius):
-    sp = synth.spec(name, N=N, B=300) if name != "serve_small" else synth.spec(name, N=N, B=500)
+# d = 1280 and 2176: the query preparation's widest register-resident form and its two-pass form
+@pytest.mark.parametrize("name,N,bits,radius,d", [("tiny", 3000, 64, 12, None), ("mid", 20000, 256, 64, None),
+                                                  ("mid_paper", 10000, 128, 30, None),
+                                                  ("serve_small", 30000, 256, 64, None), ("mid", 4000, 128, 30, 1280),
+                                                  ("mid", 3000, 64, 16, 2176)])
+def test_lsh_parity(lc, name, N, bits, radius, d):
+    extra = {} if d is None else {"d": d}
+    sp = synth.spec(name, N=N, B=300, **extra) if name != "serve_small" else synth.spec(name, N=N, B=500)
     w = synth.generate(sp)
-    say(f"[case] lsh {name} N={N} bits={bits} radius={radius}")
+    say(f"[case] lsh {name} N={N} d={sp.d} bits={bits} radius={radius}")
     g, o, gsig, sk, pk, sq, pq, kq, qq = _lsh_run(lc, sp, w, bits, radius, insert_chunk=7777)
     flips = _check_signatures(gsig, sk, pk)
     ex = _check_lookup(g, o, sk, pk, sq, pq, kq, qq, radius, sp)
