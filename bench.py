@@ -591,10 +591,10 @@ def run_large_interleaved(lc, torch, synth, epochs=8, per_epoch=8, batch=4096):
 
 def run_sweep(steps, warmup, lc, torch, synth):
     """Lookup throughput over the batch size on the 1M x 768 serving cache: the exact path at the default
-    crossover (the streaming kernel up to two 64-query groups, the GEMM kernel above) and, up to 1024
+    crossover (the streaming kernel up to three 64-query groups, the GEMM kernel above) and, up to 1024
     queries, the LSH path (256 bits, radius 64); then, for 160-256 queries, the exact path with the
-    streaming kernel forced (three and four query groups, `set_small_batch(256)`), the measurement behind
-    the default crossover.  Prints one JSON line per batch size and path set."""
+    streaming kernel forced (three and four query groups, `set_small_batch(256)`) and, for 128-256, with the
+    GEMM kernel forced (`set_small_batch(0)`): the measurements behind the default crossover.  Prints one JSON line per batch size and path set."""
     from tests.gpu_util import gpu_cache, to_dev
     sp = synth.spec("serve_large")
     w = synth.generate(sp)
@@ -647,6 +647,11 @@ def run_sweep(steps, warmup, lc, torch, synth):
     c.set_small_batch(256)  # the streaming kernel's largest batch at d = 768
     for B in (160, 192, 224, 256):
         res = {"B": B, "exact_stream_forced": measure(B, "exact")}
+        print(json.dumps(res), flush=True)
+        rows.append(res)
+    c.set_small_batch(0)  # every batch on the GEMM kernel
+    for B in (128, 160, 192, 224, 256):
+        res = {"B": B, "exact_gemm_forced": measure(B, "exact")}
         print(json.dumps(res), flush=True)
         rows.append(res)
     c.close()

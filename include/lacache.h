@@ -268,9 +268,9 @@ int lacache_export_signatures(lacache_t h, int64_t first, int32_t n, uint32_t *s
  * bandwidth-bound streaming kernel, larger ones the matrix-core GEMM kernel.
  * The streaming kernel runs up to four groups of 64 queries (fewer queries
  * per group for d > 1152); 0 <= b_small <= its largest batch, 256 for
- * d <= 1152, else EINVAL.  The default is two groups (128 queries for
- * d <= 1152): past that each CU's share of the contraction, not the key
- * reads, limits the streaming kernel and the GEMM kernel is as fast or
+ * d <= 1152, else EINVAL.  The default is three groups (192 queries for
+ * d <= 1152): from four groups on each CU's share of the contraction, not
+ * the key reads, limits the streaming kernel and the GEMM kernel is
  * faster.  0 sends every batch to the GEMM kernel.  Both kernels give the
  * same results up to float32 summation order.
  */

@@ -117,7 +117,7 @@ def _check_lookup(g, o, sk, pk, sq, pq, kq, qq, radius, sp):
 @pytest.mark.parametrize("name,N,bits,radius,d", [("tiny", 3000, 64, 12, None), ("mid", 20000, 256, 64, None),
                                                   ("mid_paper", 10000, 128, 30, None),
                                                   ("serve_small", 30000, 256, 64, None), ("mid", 4000, 128, 30, 1280),
-                                                  ("mid", 3000, 64, 16, 2176)])
+                                                  ("mid", 3000, 128, 30, 2176)])
 def test_lsh_parity(lc, name, N, bits, radius, d):
     extra = {} if d is None else {"d": d}
     sp = synth.spec(name, N=N, B=300, **extra) if name != "serve_small" else synth.spec(name, N=N, B=500)

@@ -218,15 +218,16 @@ def _edge(lc, N, d, B, k_cap, k, dtype=oracle.F32, seed=0, b_small=None, neg=Fal
     return w, g, o
 
 
-# b_small None keeps the default crossover (two streaming query groups, 128 queries for d <= 1152)
+# b_small None keeps the default crossover (three streaming query groups, 192 queries for d <= 1152)
 @pytest.mark.parametrize("N,d,B,k_cap,k,b_small", [
     (1, 64, 5, 1, 1, None),          # a single entry
     (17, 64, 16, 8, 8, None),        # one live row in the last 16-row group
     (255, 100, 17, 150, 150, None),  # d not a multiple of 128, k > 64 (two ballot rounds), ragged B
     (257, 384, 63, 20, 1, None),     # k = 1
     (1000, 384, 65, 64, 64, None),   # B just past one streaming query group: two groups of 64
-    (2000, 768, 128, 16, 16, None),  # two full streaming query groups, the default limit
-    (1000, 384, 129, 64, 64, None),  # just past the default limit: the GEMM path
+    (2000, 768, 128, 16, 16, None),  # two full streaming query groups
+    (1000, 384, 129, 64, 64, None),  # three streaming query groups, the last holding one query
+    (1000, 384, 193, 64, 64, None),  # just past the default limit: the GEMM path
     (1500, 768, 200, 16, 16, 256),   # four streaming query groups, the last one ragged
     (1000, 1152, 256, 64, 64, 256),  # the largest streaming batch, at the largest d it holds
     (900, 1280, 150, 8, 8, 192),     # d > 1152: groups of 48 queries, four of them, the last holding 6
