@@ -25,15 +25,15 @@ namespace lacache {
 // each batch without branches, so the chain of MFMAs waits for memory about kc / 8 times rather than once per
 // step.
 template <int S>
-__device__ __forceinline__ void replay_batch(const u32x4* __restrict__ kp, const u32x4* __restrict__ qp, int st0,
-                                             int lane, f32x16& acc) {
+__device__ __forceinline__ void replay_batch(const u32x4* __restrict__ kp, const u32x4* __restrict__ qp, bool qlane,
+                                             int st0, int lane, f32x16& acc) {
     u32x4 ka[S], qa[S];
 #pragma unroll
     for (int u = 0; u < S; ++u) {
         const int st = st0 + u;
         const int off = (st >> 1) * 64 + (((st & 1) << 1) + (lane >> 5)) * 16;
         ka[u] = kp[off];
-        qa[u] = qp[off];
+        qa[u] = qlane ? qp[off] : u32x4{0u, 0u, 0u, 0u};
     }
     __builtin_amdgcn_sched_barrier(0);  // every load of the batch issued before the first MFMA waits
 #pragma unroll
@@ -46,11 +46,14 @@ __device__ inline int32_t replay_group(const u32x4* __restrict__ keys, const u32
     const int qr = (b & ~31) + (lane & 31);    // query row of the fragment (column operand)
     const u32x4* kp = keys + (int64_t)(kr >> 4) * kc * 64 + (kr & 15);
     const u32x4* qp = qt + (int64_t)(qr >> 4) * kc * 64 + (qr & 15);
+    // only query b's column of the fragment is needed: every output column of the MFMA depends on its own
+    // column of the column operand alone, so the other lanes feed zeros instead of loading their queries
+    const bool qlane = (lane & 31) == (b & 31);
     f32x16 acc = f32x16{};
     const int n = 2 * kc;
     int st0 = 0;
-    for (; st0 + 16 <= n; st0 += 16) replay_batch<16>(kp, qp, st0, lane, acc);
-    if (st0 < n) replay_batch<8>(kp, qp, st0, lane, acc);
+    for (; st0 + 16 <= n; st0 += 16) replay_batch<16>(kp, qp, qlane, st0, lane, acc);
+    if (st0 < n) replay_batch<8>(kp, qp, qlane, st0, lane, acc);
     int row = 0x7FFFFFFF;
     if ((lane & 31) == (b & 31)) {
 #pragma unroll
