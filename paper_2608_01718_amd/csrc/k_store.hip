@@ -39,7 +39,8 @@ __global__ __launch_bounds__(256) void k_normalise_rows(const void* __restrict__
     }
 }
 
-// The tiled layout (keys, staged queries) for any d, one workgroup of 4 waves per 16-row group of the destination
+// The tiled layout for any d (inserts of more than kTiledRowsMax keys, and every call past d_pad = 2048), one
+// workgroup of 4 waves per 16-row group of the destination
 // (grid-stride over the groups): the waves first take the norms of the group's rows (row_norm, as above),
 // then each wave writes whole 1 KiB chunks -- lane l holds row l % 16, columns 8 (l / 16) .. +7 of the chunk --
 // so every store is one contiguous wave access.  Destination rows outside [row0, row0 + rows_pad) belong
@@ -76,12 +77,12 @@ __global__ __launch_bounds__(256) void k_normalise_tiled(const void* __restrict_
     }
 }
 
-// The tiled layout for d_pad <= 512 NC: one workgroup of 16 waves per 16-row group (grid-stride over the
-// groups), wave i on row i of the group.  Each wave reads its row once into registers, rounds it as above and
+// The tiled layout for d_pad <= 512 NC and calls of up to kTiledRowsMax rows (query staging, small inserts):
+// one workgroup of 16 waves per 16-row group (grid-stride over the groups), wave i on row i of the group.  Each wave reads its row once into registers, rounds it as above and
 // puts the 16-byte pieces into LDS, piece J (columns 8 J .. 8 J + 7) of row i at slot 16 J + (i ^ (J % 16)):
 // the XOR keeps both the row-wise writes and the chunk-wise reads on distinct banks.  Then the waves write
 // whole 1 KiB chunks as above.  With a wave per row, a group costs one read of each row and a few
-// round trips, whether the call stages 16 queries or inserts a million rows.
+// round trips: 16 queries are staged in ~5 us.
 template <int NC>
 __global__ __launch_bounds__(1024) void k_normalise_tiled_rows(const void* __restrict__ in, int dtype, int64_t rows,
                                                                int64_t rows_pad, int d, int d_pad,
