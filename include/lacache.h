@@ -286,6 +286,20 @@ int lacache_set_small_batch(lacache_t h, int32_t b_small);
 int lacache_profile(lacache_t h, int32_t enable);
 int lacache_profile_read(lacache_t h, double *stage1_ms, int64_t *lookups);
 
+/*
+ * Health counter of the large-batch stage 1.  Its GEMM kernel reports, per
+ * query, the 16-row group holding the best score; the exact row is then
+ * recovered by recomputing that group's 16 scores with the same matrix
+ * instruction sequence and taking the lowest row whose score equals the
+ * reported one (lowest index on ties, Algorithm 1's single hit entry).  If no
+ * row reproduces the score, the lowest row at the recomputed maximum is
+ * taken instead, so the lookup still names a valid entry, and this counter
+ * is incremented.  *count (host pointer) receives the number of such queries
+ * since create; it is 0 in correct operation.  Synchronises the device.
+ * Errors: EINVAL for a null handle or pointer, EHIP.
+ */
+int lacache_replay_fallbacks(lacache_t h, int64_t *count);
+
 /* Static text for a return code. */
 const char *lacache_strerror(int code);
 

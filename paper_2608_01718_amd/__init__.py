@@ -50,6 +50,7 @@ _lib.lacache_export.argtypes = [_P, _i64, _i32, _P, _P, _P, _P]
 _lib.lacache_set_small_batch.argtypes = [_P, _i32]
 _lib.lacache_profile.argtypes = [_P, _i32]
 _lib.lacache_profile_read.argtypes = [_P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_i64)]
+_lib.lacache_replay_fallbacks.argtypes = [_P, ctypes.POINTER(_i64)]
 _lib.lacache_strerror.argtypes = [ctypes.c_int]
 _lib.lacache_strerror.restype = ctypes.c_char_p
 
@@ -58,7 +59,7 @@ EXPORTED = ("lacache_create", "lacache_create_ensemble", "lacache_models", "laca
             "lacache_export", "lacache_export_prefix", "lacache_calibrate", "lacache_accept_length",
             "lacache_enable_lsh", "lacache_lookup_lsh", "lacache_export_signatures",
             "lacache_set_small_batch",
-            "lacache_profile", "lacache_profile_read", "lacache_strerror")
+            "lacache_profile", "lacache_profile_read", "lacache_replay_fallbacks", "lacache_strerror")
 
 
 class LaCacheError(RuntimeError):
@@ -173,6 +174,9 @@ class LaCache:
 
     def profile_read(self):
         return lacache_profile_read(self)
+
+    def replay_fallbacks(self) -> int:
+        return lacache_replay_fallbacks(self)
 
     def close(self) -> None:
         if getattr(self, "_h", None) is not None:
@@ -403,6 +407,14 @@ def lacache_profile_read(c: LaCache):
     ms, n = ctypes.c_double(0), _i64(0)
     _check(_lib.lacache_profile_read(c.handle, ctypes.byref(ms), ctypes.byref(n)), "lacache_profile_read")
     return ms.value, n.value
+
+
+def lacache_replay_fallbacks(c: LaCache) -> int:
+    """Queries since create whose large-batch group replay did not reproduce their stage-1 score (0 in correct
+    operation); synchronises the device."""
+    n = _i64(0)
+    _check(_lib.lacache_replay_fallbacks(c.handle, ctypes.byref(n)), "lacache_replay_fallbacks")
+    return n.value
 
 
 def raw_library() -> ctypes.CDLL:

@@ -26,12 +26,13 @@ struct lacache_s {
     int num_cu = 0, b_small = 128;
     int m = 1;                 // prefix models (lookahead checks) per entry
     int d_resp[kMaxModels] = {}, d_pad_resp[kMaxModels] = {};
-    uint16_t* keys = nullptr;  // tiled [cap_pad][d_pad]
+    uint16_t* keys = nullptr;  // tiled [cap_pad][d_pad]: whole GEMM key tiles plus one spare tile of zero rows
     uint16_t* emb[kMaxModels] = {};  // row-major [cap][d_pad_resp[i]], one per prefix model
     int32_t* tokens = nullptr; // [cap][k_cap]
     uint16_t* qt = nullptr;    // tiled [mb_pad][d_pad] normalised queries
     uint64_t* part = nullptr;  // [max_batch][kMaxPartials] packed top-1 candidates
     uint32_t* calib = nullptr; // [kCalibScratchWords] state and histograms of the calibration select
+    uint32_t* fallbacks = nullptr;  // [1] queries whose stage-1 group replay missed its score (see k_verify.hip)
     // LSH index (lacache_enable_lsh): hyperplanes, key and query signatures, candidate lists
     int lsh_bits = 0, lsh_max_cand = 0;
     uint16_t* hp = nullptr;        // tiled [lsh_bits][d_pad] raw hyperplanes
@@ -46,7 +47,7 @@ struct lacache_s {
 namespace {
 
 constexpr int64_t kMaxCapacity = (int64_t(1) << 31) - 256;
-constexpr int kRowTile = 256;  // stage-1 GEMM tile: key rows and query rows are padded to it
+constexpr int kRowTile = 256;  // query scratch rows are padded to it
 
 int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
@@ -83,6 +84,7 @@ void free_all(lacache_s* h) {
     (void)hipFree(h->qt);
     (void)hipFree(h->part);
     (void)hipFree(h->calib);
+    (void)hipFree(h->fallbacks);
     for (auto& p : h->prof) {
         (void)hipEventDestroy(p.first);
         (void)hipEventDestroy(p.second);
@@ -145,7 +147,7 @@ int lacache_create_ensemble(lacache_t* out, int64_t capacity, int32_t d, int32_t
     if (!h) return LACACHE_ENOMEM;
     h->device = device;
     h->cap = capacity;
-    h->cap_pad = round_up(capacity, kRowTile);
+    h->cap_pad = round_up(capacity, kGemmKeyTile) + kGemmKeyTile;
     h->d = d;
     h->d_pad = (int)round_up(d, 128);
     h->m = m;
@@ -173,6 +175,7 @@ int lacache_create_ensemble(lacache_t* out, int64_t capacity, int32_t d, int32_t
     if (rc == LACACHE_OK) rc = alloc_zero((void**)&h->qt, (size_t)h->mb_pad * h->d_pad * 2);
     if (rc == LACACHE_OK) rc = alloc_zero((void**)&h->part, (size_t)h->max_batch * kMaxPartials * 8);
     if (rc == LACACHE_OK) rc = alloc_zero((void**)&h->calib, (size_t)kCalibScratchWords * 4);
+    if (rc == LACACHE_OK) rc = alloc_zero((void**)&h->fallbacks, 4);
     if (rc == LACACHE_OK && hipDeviceSynchronize() != hipSuccess) rc = LACACHE_EHIP;
     if (rc != LACACHE_OK) {
         free_all(h);
@@ -247,7 +250,8 @@ static int lookup_chunk(lacache_t h, const char* queries, const PrefixModels& mo
     if (n_rows > 0) {
         // the streaming kernel runs more than one query group on whole groups of 16 * stream_max_qg rows
         const int64_t grp = 16 * (int64_t)stream_max_qg(h->d_pad);
-        const int64_t rows_pad = small ? (B <= grp ? round_up(B, 16) : round_up(B, grp)) : round_up(B, kRowTile);
+        const int64_t rows_pad =
+            small ? (B <= grp ? round_up(B, 16) : round_up(B, grp)) : round_up(B, kGemmQueryTile);
         if (launch_normalise(queries, h->dtype, B, rows_pad, h->d, h->d_pad, h->qt, 0, true, s) != hipSuccess)
             return LACACHE_EHIP;
         hipEvent_t e0 = nullptr, e1 = nullptr;
@@ -262,7 +266,7 @@ static int lookup_chunk(lacache_t h, const char* queries, const PrefixModels& mo
         if (h->profiling && hipEventRecord(e1, s) != hipSuccess) return LACACHE_EHIP;
     }
     if (launch_finalize_verify(h->part, P, !small, h->keys, h->qt, B, n_rows, h->dtype, h->d, models, la_tok, k,
-                               h->tokens, h->k_cap, tau_q, idx, score, resp, dec, s) != hipSuccess)
+                               h->tokens, h->k_cap, tau_q, idx, score, resp, dec, h->fallbacks, s) != hipSuccess)
         return LACACHE_EHIP;
     return LACACHE_OK;
 }
@@ -438,6 +442,17 @@ int lacache_export_signatures(lacache_t h, int64_t first, int32_t n, uint32_t* s
     if (hipMemcpyAsync(sig, h->sig + first * words, (size_t)n * words * 4, hipMemcpyDeviceToDevice,
                        (hipStream_t)stream) != hipSuccess)
         return LACACHE_EHIP;
+    return LACACHE_OK;
+}
+
+int lacache_replay_fallbacks(lacache_t h, int64_t* count) {
+    if (!h || !count) return LACACHE_EINVAL;
+    DeviceGuard g(h->device);
+    if (!g.ok) return LACACHE_EHIP;
+    uint32_t v = 0;
+    if (hipDeviceSynchronize() != hipSuccess || hipMemcpy(&v, h->fallbacks, 4, hipMemcpyDeviceToHost) != hipSuccess)
+        return LACACHE_EHIP;
+    *count = v;
     return LACACHE_OK;
 }
 

@@ -44,10 +44,13 @@ hipError_t launch_export(const uint16_t* src, int64_t first, int n, int d, int d
 hipError_t launch_stage1_stream(const uint16_t* keys, const uint16_t* qt, int B, int n_rows, int d_pad,
                                 uint64_t* part, int num_cu, int* P_out, hipStream_t s);
 
-// Stage 1, compute-bound path (matrix-core GEMM with a fused row maximum):
-// queries qt (tiled, rows padded to a multiple of 256) against n_rows keys.  Its partials name the
-// 32-row group of the candidate (global row / 32) instead of the row; the finalize step recovers the
-// row by replaying that group (part_groups = true).
+// Stage 1, compute-bound path (matrix-core GEMM with a fused row maximum): queries qt (tiled, rows zero-padded
+// to a multiple of kGemmQueryTile) against n_rows keys.  The key store must hold whole tiles of kGemmKeyTile
+// rows plus one spare tile past the last one (the kernel prefetches into it; its rows are never scored).  Its
+// partials name the 16-row group of the candidate (global row / 16) instead of the row; the finalize step
+// recovers the row by replaying that group (part_groups = true).
+constexpr int kGemmKeyTile = 512;
+constexpr int kGemmQueryTile = 128;
 hipError_t launch_stage1_gemm(const uint16_t* keys, const uint16_t* qt, int B, int n_rows, int d_pad,
                               uint64_t* part, int num_cu, int* P_out, hipStream_t s);
 
@@ -61,13 +64,14 @@ struct PrefixModels {
     float tau[kMaxModels];             // stage-2 threshold of each model
 };
 
-// Merge the P partial candidates of each query (rows, or 32-row groups to replay against keys_tiled and
-// the tiled queries qt), threshold, and run stage 2 on hits.  resp_score is [B][models.m].
+// Merge the P partial candidates of each query (rows, or 16-row groups to replay against keys_tiled and
+// the tiled queries qt), threshold, and run stage 2 on hits.  resp_score is [B][models.m].  Every query whose
+// group replay does not reproduce its stage-1 score adds 1 to *fallbacks (device memory).
 hipError_t launch_finalize_verify(const uint64_t* part, int P, bool part_groups, const uint16_t* keys_tiled,
                                   const uint16_t* qt, int B, int n_rows, int dtype, int d_keys,
                                   const PrefixModels& models, const int32_t* la_tok, int k, const int32_t* tokens,
                                   int k_cap, float tau_q, int32_t* idx, float* score, float* resp_score,
-                                  int32_t* decision, hipStream_t s);
+                                  int32_t* decision, uint32_t* fallbacks, hipStream_t s);
 
 // Threshold calibration over n pairs (a[j], b[j]) of d-dimensional input vectors: sims[j] = the lookup's
 // cosine of the pair; tau[0] = the percentile (linear between the closest ranks), tau[1] = min(cap, tau[0]).

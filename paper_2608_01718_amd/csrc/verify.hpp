@@ -17,54 +17,92 @@
 
 namespace lacache {
 
-// Exact row of query b inside the 32-row group g that the GEMM path reported: replay the group against
-// the same 32-query fragment with the same MFMA sequence (v_mfma_f32_32x32x16_bf16 over the 16-column
-// steps in order, from a zero accumulator), which reproduces the GEMM's float32 scores bit for bit, and
-// take the lowest stored row whose score equals s.  Returns -1 if none does.  The operand fragments are
-// loaded 16 steps at a time (the 2 kc steps are a multiple of 8: full batches of 16, then at most one of 8),
-// each batch without branches, so the chain of MFMAs waits for memory about kc / 8 times rather than once per
-// step.
+// The row a group replay names, and the rule that picks it (host-callable, so the rule itself is checked on the
+// CPU): the lowest row whose replayed score equals the stage-1 score; if none does (the replay did not
+// reproduce the stage-1 arithmetic), the lowest row at the replay's own maximum, flagged as a fallback, so that
+// a valid entry of the group is always returned.  Rows are offered one at a time (replay_pick_add) and the
+// partial picks of several lanes merged in any order (replay_pick_merge).
+struct ReplayPick {
+    int exact;    // lowest row whose replayed score equals the stage-1 score (0x7FFFFFFF: none)
+    float top;    // highest replayed score seen
+    int top_row;  // lowest row holding it (0x7FFFFFFF: no row seen)
+};
+__host__ __device__ inline ReplayPick replay_pick_none() { return ReplayPick{0x7FFFFFFF, -__builtin_inff(), 0x7FFFFFFF}; }
+__host__ __device__ inline ReplayPick replay_pick_add(ReplayPick p, int row, float v, float s) {
+    if (v == s && row < p.exact) p.exact = row;
+    if (v > p.top || (v == p.top && row < p.top_row)) {
+        p.top = v;
+        p.top_row = row;
+    }
+    return p;
+}
+__host__ __device__ inline ReplayPick replay_pick_merge(ReplayPick a, ReplayPick b) {
+    ReplayPick r;
+    r.exact = a.exact < b.exact ? a.exact : b.exact;
+    const bool take_b = b.top > a.top || (b.top == a.top && b.top_row < a.top_row);
+    r.top = take_b ? b.top : a.top;
+    r.top_row = take_b ? b.top_row : a.top_row;
+    return r;
+}
+// The named row (-1 when no row was offered); *fallback is set when no replayed score matched.
+__host__ __device__ inline int replay_pick_row(ReplayPick p, bool* fallback) {
+    *fallback = p.exact == 0x7FFFFFFF;
+    const int r = *fallback ? p.top_row : p.exact;
+    return r == 0x7FFFFFFF ? -1 : r;
+}
+
+// Exact row of query b inside the 16-row group g that the GEMM path reported: replay the group against query
+// b with the stage-1 instruction sequence (v_mfma_f32_16x16x32_bf16 over the 32-column steps in order, from a
+// zero accumulator), which reproduces the GEMM's float32 scores bit for bit, and pick the row with
+// replay_pick_*.  The key operand is the group's 1 KiB chunk of each step; only query b's column of the query
+// operand is loaded (every output column of the MFMA depends on its own column alone), the other lanes feed
+// zeros.  The operand fragments are loaded 8 steps at a time (kc is a multiple of 4: full batches of 8, then at
+// most one of 4), each batch without branches, so the chain of MFMAs waits for memory about kc / 8 times.
 template <int S>
-__device__ __forceinline__ void replay_batch(const u32x4* __restrict__ kp, const u32x4* __restrict__ qp, bool qlane,
-                                             int st0, int lane, f32x16& acc) {
+__device__ __forceinline__ void replay16_batch(const u32x4* __restrict__ kp, const u32x4* __restrict__ qp, bool qlane,
+                                               int st0, f32x4& acc) {
     u32x4 ka[S], qa[S];
 #pragma unroll
     for (int u = 0; u < S; ++u) {
-        const int st = st0 + u;
-        const int off = (st >> 1) * 64 + (((st & 1) << 1) + (lane >> 5)) * 16;
-        ka[u] = kp[off];
-        qa[u] = qlane ? qp[off] : u32x4{0u, 0u, 0u, 0u};
+        ka[u] = kp[(int64_t)(st0 + u) * 64];
+        qa[u] = qlane ? qp[(int64_t)(st0 + u) * 64] : u32x4{0u, 0u, 0u, 0u};
     }
     __builtin_amdgcn_sched_barrier(0);  // every load of the batch issued before the first MFMA waits
 #pragma unroll
-    for (int u = 0; u < S; ++u) acc = mfma32x32x16(ka[u], qa[u], acc);
+    for (int u = 0; u < S; ++u) acc = mfma16x16x32(ka[u], qa[u], acc);
 }
 
-__device__ inline int32_t replay_group(const u32x4* __restrict__ keys, const u32x4* __restrict__ qt, int kc, int b, int g,
-                                float s, int n_rows, int lane) {
-    const int kr = g * 32 + (lane & 31);       // key row this lane feeds (row operand)
-    const int qr = (b & ~31) + (lane & 31);    // query row of the fragment (column operand)
-    const u32x4* kp = keys + (int64_t)(kr >> 4) * kc * 64 + (kr & 15);
-    const u32x4* qp = qt + (int64_t)(qr >> 4) * kc * 64 + (qr & 15);
-    // only query b's column of the fragment is needed: every output column of the MFMA depends on its own
-    // column of the column operand alone, so the other lanes feed zeros instead of loading their queries
-    const bool qlane = (lane & 31) == (b & 31);
-    f32x16 acc = f32x16{};
-    const int n = 2 * kc;
+__device__ inline int32_t replay_group16(const u32x4* __restrict__ keys, const u32x4* __restrict__ qt, int kc, int b,
+                                         int g, float s, int n_rows, int lane, bool* fallback) {
+    const u32x4* kp = keys + (int64_t)g * kc * 64 + lane;          // chunk (g, j) at kp + 64 j
+    const u32x4* qp = qt + (int64_t)(b >> 4) * kc * 64 + lane;     // query rows (b & ~15) .. + 15
+    const bool qlane = (lane & 15) == (b & 15);
+    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
     int st0 = 0;
-    for (; st0 + 16 <= n; st0 += 16) replay_batch<16>(kp, qp, qlane, st0, lane, acc);
-    if (st0 < n) replay_batch<8>(kp, qp, qlane, st0, lane, acc);
-    int row = 0x7FFFFFFF;
-    if ((lane & 31) == (b & 31)) {
+    for (; st0 + 8 <= kc; st0 += 8) replay16_batch<8>(kp, qp, qlane, st0, acc);
+    if (st0 < kc) replay16_batch<4>(kp, qp, qlane, st0, acc);
+    // lane l holds rows 4 (l / 16) + i of the group for query column l % 16
+    ReplayPick p = replay_pick_none();
+    if (qlane) {
 #pragma unroll
-        for (int j = 15; j >= 0; --j) {
-            const int r = g * 32 + 8 * (j >> 2) + 4 * (lane >> 5) + (j & 3);
-            if (acc[j] == s && r < n_rows) row = r;
+        for (int i = 0; i < 4; ++i) {
+            const int r = g * 16 + 4 * (lane >> 4) + i;
+            if (r < n_rows) p = replay_pick_add(p, r, acc[i], s);
         }
     }
 #pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) row = min(row, __shfl_xor(row, m, kWave));
-    return row == 0x7FFFFFFF ? -1 : row;
+    for (int m = 16; m <= 32; m <<= 1) {
+        ReplayPick o;
+        o.exact = __shfl_xor(p.exact, m, kWave);
+        o.top = __shfl_xor(p.top, m, kWave);
+        o.top_row = __shfl_xor(p.top_row, m, kWave);
+        p = replay_pick_merge(p, o);
+    }
+    // lane b % 16 now holds the merged pick of the four lanes of query b
+    p.exact = __shfl(p.exact, b & 15, kWave);
+    p.top = __shfl(p.top, b & 15, kWave);
+    p.top_row = __shfl(p.top_row, b & 15, kWave);
+    return replay_pick_row(p, fallback);
 }
 
 // One wave: outputs of query b for the packed stage-1 result m (0: no candidate) naming entry i with raw

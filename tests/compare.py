@@ -38,7 +38,7 @@ def compare(gpu: dict, orc: dict, keys_q, emb_q, tokens, q_q, a_q, u, tau_q, tau
         assert np.all(g["idx"] == -1), g["idx"]
         assert np.all(np.isnan(g["score"])) and np.all(np.isnan(g["resp_score"]))
         assert np.all(g["decision"] == oracle.MISS)
-        return dict(n=len(rows), idx_exact=len(rows), near_tie=0, thr_margin=0)
+        return dict(n=len(rows), idx_exact=len(rows), near_tie=0, near_set=0, thr_margin=0)
 
     at = g["idx"].astype(np.int32)
     assert np.all((at >= 0) & (at < N)), f"index out of range: {at[(at < 0) | (at >= N)]}"
@@ -79,7 +79,10 @@ def compare(gpu: dict, orc: dict, keys_q, emb_q, tokens, q_q, a_q, u, tau_q, tau
     dr = np.abs(g["resp_score"][both].astype(np.float64) - dec_at["resp_score"][both])
     assert np.all(dr <= SCORE_TOL), f"resp_score off by {dr.max()}"
     assert np.all(np.abs(g["score"]) <= 1) and np.all(np.abs(g["resp_score"][~gn]) <= 1)
-    return dict(n=len(rows), idx_exact=int(same.sum()), near_tie=int((~same).sum()), thr_margin=int(thr.sum()))
+    # near_set: rows whose oracle top-2 margin is below MARGIN (the near-tie set S_b holds more than the top-1, so
+    # the idx rule is the set-membership one); near_tie: rows where the GPU's entry differs from the oracle's
+    return dict(n=len(rows), idx_exact=int(same.sum()), near_tie=int((~same).sum()), near_set=int(near.sum()),
+                thr_margin=int(thr.sum()))
 
 
 def compare_ensemble(gpu: dict, orc: dict, s1: dict, tau_q, tau_r, rows=None) -> dict:

@@ -15,7 +15,7 @@ import pytest
 import oracle
 import synth
 from tests.compare import MARGIN, SCORE_TOL, compare
-from tests.gpu_util import gpu_cache, gpu_lookup, oracle_store, to_dev
+from tests.gpu_util import gpu_cache, gpu_lookup, oracle_store, sample_rows, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -201,7 +201,8 @@ def test_lsh_edges(lc):
 def test_lsh_recall_full_size_serve(lc):
     """The serving workload at full size (1M x 768, 4096 queries): 256-bit signatures, radius 64.  Against
     the exact lookup every stage-1 hit is found (same entry, same decision) and the candidate lists stay
-    short; a sample of queries is checked against the oracle's LSH lookup."""
+    short; the exported signatures of all 1M entries and a stratified sample of 48 queries (every class) are
+    checked against the oracle's signatures and LSH lookup."""
     sp = synth.spec("serve_small")
     w = synth.generate(sp)
     bits, radius = 256, 64
@@ -213,6 +214,7 @@ def test_lsh_recall_full_size_serve(lc):
     out = c.lookup_lsh(to_dev(w.queries), to_dev(w.la_emb), to_dev(np.ascontiguousarray(w.la_tok[:, :sp.k])),
                        sp.tau_q, sp.tau_r, sp.k, radius)
     g = [t.cpu().numpy() for t in out]
+    gsig = c.export_signatures(0, sp.N).cpu().numpy().view(np.uint32)
     c.close()
     hit = ex["decision"] >= 1                                 # exact stage-1 hits
     found = (g[0] == ex["idx"]) & (g[3] == ex["decision"])
@@ -221,3 +223,18 @@ def test_lsh_recall_full_size_serve(lc):
     say(f"[ok] recall of stage-1 hits {recall_hits:.4f} ({int(hit.sum())} hits), misses kept {miss_ok:.4f}, "
         f"mean candidates {g[4].mean():.2f}, max {g[4].max()}")
     assert recall_hits >= 0.999 and miss_ok == 1.0 and g[4].max() <= 256
+    # the oracle's LSH lookup on a stratified sample
+    rows = sample_rows(w.cls, w.target, 48)
+    kq, eq, tok = oracle_store(sp, w.keys, w.emb, w.tokens)
+    qq = oracle.quantise(w.queries[rows], sp.in_dtype)
+    aq = oracle.quantise(w.la_emb[rows], sp.in_dtype)
+    u = np.ascontiguousarray(w.la_tok[rows, :sp.k])
+    sk, pk = oracle.simhash(kq, hp, bits)
+    flips = _check_signatures(gsig, sk, pk)
+    sq, pq = oracle.simhash(qq, hp, bits)
+    o = oracle.lookup_lsh(kq, eq, tok, sk, qq, sq, aq, u, radius, sp.tau_q, sp.tau_r, sp.k)
+    gs = dict(idx=g[0][rows], score=g[1][rows], resp_score=g[2][rows], decision=g[3][rows], n_cand=g[4][rows])
+    exempt = _check_lookup(gs, o, sk, pk, sq, pq, kq, qq, radius, sp)
+    say(f"[ok] lsh full size vs oracle: {len(rows)} sampled queries, exempt {exempt}, signature bit flips near "
+        f"zero {flips}, hits {int(np.sum(gs['decision'] >= 2))}")
+    assert exempt <= 2
