@@ -432,17 +432,16 @@ def test_errors_with_live_handle(lc):
     c.close()
 
 
-def test_parity_large_full_size_interleaved(lc):
-    """The large clustered workload at full size: 4,000,000 x 1024 keys (top-2 margins often below 2e-3),
-    k = 32, 1024 queries per lookup, an insert batch of 4096 entries between lookups, 10% of the planted
-    queries aimed at the latest batch; at every step 512 stratified rows (the misses, whose top-2 margins sit
-    near 2e-3, among them) and the latest-batch-aimed rows against the oracle.  The rows whose oracle top-2
-    margin is below 2e-3 -- the near-tie set, where the idx rule becomes set membership -- are counted and must
-    occur."""
+LARGE_STEPS, LARGE_BATCH = 3, 4096
+
+
+@pytest.fixture(scope="module")
+def large_state(lc):
+    """The large clustered workload at full size, shared by the serving steps below: 4,000,000 x 1024 keys
+    generated with room for LARGE_STEPS insert batches, the oracle's quantised store, and the cache."""
     import time
     sp = synth.spec("large")
-    steps, batch = 3, 4096
-    total = sp.N + steps * batch
+    total = sp.N + LARGE_STEPS * LARGE_BATCH
     t0 = time.time()
     keys, emb, tok = synth.entries(sp, 0, total)
     say(f"[case] large full size: generated {total} entries in {time.time() - t0:.1f}s")
@@ -450,32 +449,47 @@ def test_parity_large_full_size_interleaved(lc):
     say(f"[case] large full size: oracle store quantised ({time.time() - t0:.1f}s)")
     c = gpu_cache(lc, sp, keys[:sp.N], emb[:sp.N], tok[:sp.N], capacity=total, max_batch=sp.B,
                   insert_chunk=1 << 18)
-    n = sp.N
-    near_total = 0
-    for step in range(steps + 1):
-        recent = (n - batch, n) if step > 0 else None
-        q = synth.queries(sp, keys, emb, tok, np.zeros((0, 2), np.int64), B=sp.B, N=n, stream_chunk=100 + step,
-                          recent=recent)
-        g = gpu_lookup(c, q["queries"], q["la_emb"], q["la_tok"], sp.tau_q, sp.tau_r, sp.k)
-        rows = sample_rows(q["cls"], q["target"], 640, seed=step)
-        if recent is not None:
-            aimed = np.nonzero((q["target"] >= recent[0]) & (q["cls"] == synth.CLS_BENIGN))[0][:8]
-            rows = np.unique(np.concatenate([rows, aimed]))
-        qq, aq = oracle.quantise(q["queries"], sp.in_dtype), oracle.quantise(q["la_emb"], sp.in_dtype)
-        u = np.ascontiguousarray(q["la_tok"][:, :sp.k])
-        o = oracle.lookup(kq[:n], eq[:n], tq[:n], qq[rows], aq[rows], u[rows], sp.tau_q, sp.tau_r, sp.k)
-        stats = compare(g, o, kq[:n], eq[:n], tq[:n], qq, aq, u, sp.tau_q, sp.tau_r, sp.k, rows)
-        assert stats["n"] >= 512
-        near_total += stats["near_set"]
-        say(f"[ok] large step {step} N={n}: {stats} ({time.time() - t0:.1f}s)")
-        # the whole batch: planted benign queries are served, collisions rejected
-        ben, col = q["cls"] == synth.CLS_BENIGN, q["cls"] == synth.CLS_COLLISION
-        assert np.all(np.isin(g["decision"][ben], [oracle.HIT, oracle.HIT_EXACT]))
-        assert np.all(g["decision"][col] == oracle.REJECT)
-        if step < steps:
-            first = c.insert(to_dev(keys[n:n + batch]), to_dev(emb[n:n + batch]), to_dev(tok[n:n + batch]))
-            assert first == n
-            n += batch
-    assert c.replay_fallbacks() == 0
+    st = dict(sp=sp, keys=keys, emb=emb, tok=tok, kq=kq, eq=eq, tq=tq, c=c, n=sp.N, done=-1)
+    yield st
     c.close()
-    assert near_total > 0, "no sampled row had a top-2 margin below 2e-3"
+
+
+@pytest.mark.parametrize("step", list(range(LARGE_STEPS + 1)))
+def test_parity_large_full_size_interleaved(lc, large_state, step):
+    """The large clustered workload at full size: 4,000,000 x 1024 keys (top-2 margins often below 2e-3),
+    k = 32, 1024 queries per lookup, an insert batch of 4096 entries between lookups (one test per serving
+    step, in order, on one cache), 10% of the planted queries aimed at the latest batch.  At every step 512
+    stratified rows (the misses, whose top-2 margins sit near 2e-3, among them) and the latest-batch-aimed rows
+    against the oracle; the rows whose oracle top-2 margin is below 2e-3 -- the near-tie set, where the idx rule
+    becomes set membership -- are counted and must occur."""
+    st = large_state
+    assert st["done"] == step - 1, "the serving steps run in order"
+    sp, keys, emb, tok, kq, eq, tq, c = (st[k] for k in ("sp", "keys", "emb", "tok", "kq", "eq", "tq", "c"))
+    n = st["n"]
+    if step > 0:
+        first = c.insert(to_dev(keys[n:n + LARGE_BATCH]), to_dev(emb[n:n + LARGE_BATCH]),
+                         to_dev(tok[n:n + LARGE_BATCH]))
+        assert first == n
+        n += LARGE_BATCH
+        st["n"] = n
+    recent = (n - LARGE_BATCH, n) if step > 0 else None
+    q = synth.queries(sp, keys, emb, tok, np.zeros((0, 2), np.int64), B=sp.B, N=n, stream_chunk=100 + step,
+                      recent=recent)
+    g = gpu_lookup(c, q["queries"], q["la_emb"], q["la_tok"], sp.tau_q, sp.tau_r, sp.k)
+    rows = sample_rows(q["cls"], q["target"], 640, seed=step)
+    if recent is not None:
+        aimed = np.nonzero((q["target"] >= recent[0]) & (q["cls"] == synth.CLS_BENIGN))[0][:8]
+        rows = np.unique(np.concatenate([rows, aimed]))
+    qq, aq = oracle.quantise(q["queries"], sp.in_dtype), oracle.quantise(q["la_emb"], sp.in_dtype)
+    u = np.ascontiguousarray(q["la_tok"][:, :sp.k])
+    o = oracle.lookup(kq[:n], eq[:n], tq[:n], qq[rows], aq[rows], u[rows], sp.tau_q, sp.tau_r, sp.k)
+    stats = compare(g, o, kq[:n], eq[:n], tq[:n], qq, aq, u, sp.tau_q, sp.tau_r, sp.k, rows)
+    say(f"[ok] large step {step} N={n}: {stats}")
+    assert stats["n"] >= 512
+    assert stats["near_set"] > 0, "no sampled row had a top-2 margin below 2e-3"
+    # the whole batch: planted benign queries are served, collisions rejected
+    ben, col = q["cls"] == synth.CLS_BENIGN, q["cls"] == synth.CLS_COLLISION
+    assert np.all(np.isin(g["decision"][ben], [oracle.HIT, oracle.HIT_EXACT]))
+    assert np.all(g["decision"][col] == oracle.REJECT)
+    assert c.replay_fallbacks() == 0
+    st["done"] = step
