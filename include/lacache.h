@@ -207,6 +207,23 @@ int lacache_calibrate(lacache_t h, int32_t which, const void *a, const void *b, 
                       float cap, float *sims, float *tau, void *stream);
 
 /*
+ * lacache_calibrate without a handle and without allocating: for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation).  The same pair cosines, selection
+ * and outputs as lacache_calibrate, for n pairs of d-dimensional vectors of
+ * the given dtype, on the calling thread's current device and on `stream`.
+ * The selection's scratch (its state and two 2048-bin histograms, 16.6 KB)
+ * is a static array of the library's device image: one copy per GPU, held
+ * until the process ends, its size fixed whatever n and d are; it is cleared
+ * by the call itself, so calls ordered on one stream are independent, while
+ * calls that overlap on one GPU (other streams, other threads) race on it.
+ *   1 <= d <= 16384; 1 <= n <= 2^32 - 1; 0 <= percentile <= 100; cap finite;
+ * EINVAL otherwise or for a NULL pointer; EHIP for a HIP failure.
+ */
+int lacache_calibrate_noalloc(const void *a, const void *b, lacache_dtype dtype, int32_t d, int64_t n,
+                              float percentile, float cap, float *sims, float *tau, void *stream);
+
+/*
  * Speculative-decoding acceptance after a miss or a rejected lookahead
  * (Section 4.3): the k draft tokens of the draft model g are verified by the
  * target model f in one forward pass; token t_j is accepted when

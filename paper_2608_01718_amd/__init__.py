@@ -37,6 +37,7 @@ _lib.lacache_lookup_ensemble.argtypes = [_P, _P, ctypes.POINTER(_P), _P, _i32, _
                                          _P, _P, _P, _P, _P]
 _lib.lacache_export_prefix.argtypes = [_P, _i32, _i64, _i32, _P, _P]
 _lib.lacache_calibrate.argtypes = [_P, _i32, _P, _P, _i64, _f32, _f32, _P, _P, _P]
+_lib.lacache_calibrate_noalloc.argtypes = [_P, _P, ctypes.c_int, _i32, _i64, _f32, _f32, _P, _P, _P]
 _lib.lacache_accept_length.argtypes = [_P, ctypes.c_int, _i32, _P, _P, _i32, _i32, _P, _P, _P]
 _lib.lacache_enable_lsh.argtypes = [_P, _i32, _P, _i32, _P]
 _lib.lacache_lookup_lsh.argtypes = [_P, _P, _P, _P, _i32, _f32, _f32, _i32, _i32, _P, _P, _P, _P, _P, _P]
@@ -56,7 +57,8 @@ _lib.lacache_strerror.restype = ctypes.c_char_p
 
 EXPORTED = ("lacache_create", "lacache_create_ensemble", "lacache_models", "lacache_destroy", "lacache_insert",
             "lacache_insert_ensemble", "lacache_lookup", "lacache_lookup_ensemble", "lacache_size",
-            "lacache_export", "lacache_export_prefix", "lacache_calibrate", "lacache_accept_length",
+            "lacache_export", "lacache_export_prefix", "lacache_calibrate", "lacache_calibrate_noalloc",
+            "lacache_accept_length",
             "lacache_enable_lsh", "lacache_lookup_lsh", "lacache_export_signatures",
             "lacache_set_small_batch",
             "lacache_profile", "lacache_profile_read", "lacache_replay_fallbacks", "lacache_strerror")
@@ -323,6 +325,28 @@ def lacache_calibrate(c: LaCache, which: int, a, b, percentile: float, cap: floa
     _check(_lib.lacache_calibrate(c.handle, int(which), _vec(a, c.in_dtype, n, dim, c.device, "a"),
                                   _vec(b, c.in_dtype, n, dim, c.device, "b"), n, float(percentile), float(cap),
                                   sims.data_ptr(), tau.data_ptr(), _stream(c.device, stream)), "lacache_calibrate")
+    return out
+
+
+def lacache_calibrate_noalloc(a, b, percentile: float, cap: float, out=None, stream=None):
+    """lacache_calibrate without a handle, with the library's static scratch: a, b [n][d] float32 or bfloat16
+    (int16/uint16 bits) on the current device.  Returns (sims f32 [n], tau f32 [2]); with `out` given no device
+    memory is allocated here either."""
+    if a.dim() != 2 or a.shape != b.shape or a.dtype != b.dtype:
+        raise ValueError("a, b: expected two [n, d] tensors of one dtype")
+    dtype = F32 if a.dtype == torch.float32 else BF16
+    n, d = a.shape
+    dev = a.device
+    if out is None:
+        out = (torch.empty(n, dtype=torch.float32, device=dev), torch.empty(2, dtype=torch.float32, device=dev))
+    sims, tau = out
+    for t, k, nm in ((sims, n, "sims"), (tau, 2, "tau")):
+        if t.dtype != torch.float32 or t.device != dev or t.numel() != k or not t.is_contiguous():
+            raise ValueError(f"{nm}: expected a contiguous float32 tensor of {k} elements on {dev}")
+    _check(_lib.lacache_calibrate_noalloc(_vec(a, dtype, n, d, dev.index, "a"), _vec(b, dtype, n, d, dev.index, "b"),
+                                          dtype, d, n, float(percentile), float(cap), sims.data_ptr(),
+                                          tau.data_ptr(), _stream(dev.index, stream)),
+           "lacache_calibrate_noalloc")
     return out
 
 

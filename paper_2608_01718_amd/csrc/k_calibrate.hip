@@ -12,6 +12,8 @@
 // histogram passes over the orderable 32-bit keys of the similarities (11,
 // 11 and 10 bits), each followed by a one-workgroup scan that fixes those
 // bits of both ranks' keys.
+#include <mutex>
+
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -200,6 +202,33 @@ __global__ void k_select_final(const uint32_t* __restrict__ state, double frac, 
     const double P = lo + frac * (hi - lo);
     out[0] = (float)P;
     out[1] = (float)fmin((double)cap, P);
+}
+
+// Scratch of the allocation-free calibration entry point (lacache_calibrate_noalloc): the selection's state
+// and histograms, kCalibScratchWords words.  Every GPU the library runs on holds its own copy for the life of
+// the process; all such calls on one GPU share it (k_select_init clears it at the start of each call, so calls
+// ordered on one stream are independent; calls that overlap on one GPU race).
+static __device__ __align__(256) uint32_t scratch[kCalibScratchWords];
+
+hipError_t calibrate_static_scratch(uint32_t** out) {
+    // the array's device address, taken once per device with that device current (the host-side name of the
+    // array is no device address); devices past the cache's range look it up on every call
+    static std::mutex mu;
+    static uint32_t* addr[64] = {};
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    std::lock_guard<std::mutex> lock(mu);
+    if (dev >= 0 && dev < 64 && addr[dev]) {
+        *out = addr[dev];
+        return hipSuccess;
+    }
+    uint32_t* p = nullptr;
+    e = hipGetSymbolAddress((void**)&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (dev >= 0 && dev < 64) addr[dev] = p;
+    *out = p;
+    return hipSuccess;
 }
 
 hipError_t launch_calibrate(const void* a, const void* b, int dtype, int d, int64_t n, float percentile, float cap,

@@ -358,6 +358,24 @@ int lacache_calibrate(lacache_t h, int32_t which, const void* a, const void* b, 
     return LACACHE_OK;
 }
 
+int lacache_calibrate_noalloc(const void* a, const void* b, lacache_dtype dtype, int32_t d, int64_t n, float percentile,
+                              float cap, float* sims, float* tau, void* stream) {
+    if ((dtype != LACACHE_F32 && dtype != LACACHE_BF16) || d < 1 || d > 16384 || n < 1 || n > (int64_t)UINT32_MAX ||
+        !std::isfinite(percentile) || percentile < 0.0f || percentile > 100.0f || !std::isfinite(cap) || !a || !b ||
+        !sims || !tau)
+        return LACACHE_EINVAL;
+    int dev = 0, num_cu = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&num_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        return LACACHE_EHIP;
+    uint32_t* scratch = nullptr;
+    if (calibrate_static_scratch(&scratch) != hipSuccess) return LACACHE_EHIP;
+    if (launch_calibrate(a, b, (int)dtype, d, n, percentile, cap, sims, tau, scratch, num_cu, (hipStream_t)stream) !=
+        hipSuccess)
+        return LACACHE_EHIP;
+    return LACACHE_OK;
+}
+
 int lacache_accept_length(const void* logits, lacache_dtype dtype, int32_t V, const int32_t* draft_tokens,
                           const float* p_draft, int32_t B, int32_t k, int32_t* accept_len, float* p_target,
                           void* stream) {

@@ -80,6 +80,10 @@ constexpr int kCalibScratchWords = 64 + 2 * 2048;
 hipError_t launch_calibrate(const void* a, const void* b, int dtype, int d, int64_t n, float percentile, float cap,
                             float* sims, float* tau, uint32_t* scratch, int num_cu, hipStream_t s);
 
+// Device address, on the current device, of the library's static calibration scratch (kCalibScratchWords words,
+// one copy per device, shared by every allocation-free calibration on that device).  Allocates nothing.
+hipError_t calibrate_static_scratch(uint32_t** out);
+
 // Speculative-decoding acceptance: p_target[b][j] = softmax(logits[b][j])[tokens[b][j]] (0 for an
 // out-of-range token); accept_len[b] = the number of leading positions with p_target >= p_draft.
 hipError_t launch_accept_length(const void* logits, int dtype, int V, const int32_t* tokens, const float* p_draft,
