@@ -54,6 +54,12 @@ MUTANTS = {
                                                                    "if (p > 0.0)\n                sig[j * words"),
     "candidates strictly inside the radius": ("words) > radius)", "words) >= radius)"),
     "Hamming distance from OR instead of XOR": ("__builtin_popcount(a[w] ^ b[w])", "__builtin_popcount(a[w] | b[w])"),
+    "an exact-tie copy names itself": ("            return j;\n    return i;", "            return i;\n    return i;"),
+    "the copy search compares one element too few": (
+        "memcmp(keys + j * (int64_t)d, ki, (size_t)d * sizeof(uint16_t))",
+        "memcmp(keys + j * (int64_t)d, ki, (size_t)(d - 1) * sizeof(uint16_t))"),
+    "the copy search starts after the first row": ("for (int64_t j = 0; j < i; ++j)\n        if (memcmp",
+                                                   "for (int64_t j = 1; j < i; ++j)\n        if (memcmp"),
     "probability read at the next vocabulary entry": ("exp(read_in(logits, dtype, row, V, t) - m) / s",
                                                       "exp(read_in(logits, dtype, row, V, (t + 1) % V) - m) / s"),
 }

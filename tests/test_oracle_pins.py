@@ -274,6 +274,38 @@ def test_self_query_returns_itself_with_unit_score():
     np.testing.assert_array_equal(out["decision"], HIT_EXACT)
 
 
+def test_first_identical_against_bruteforce():
+    """The lowest index whose stored key is bitwise identical to entry i (the exact-tie rule's reference):
+    copies planted at known positions -- a later copy names its earliest original, including chains of three
+    copies, a copy of the store's first row and a copy that is its last row -- against a brute force over the whole store; a unique row
+    names itself; a row differing from another in a single bf16 ulp (in a middle or the last element), or by
+    the sign of a zero, is no copy;
+    an index outside the store names -1."""
+    rng = np.random.default_rng(91)
+    N, d = 400, 37
+    kq = oracle.quantise(rng.standard_normal((N, d)).astype(np.float32), oracle.F32)
+    kq[57] = kq[12]                       # a plain copy
+    kq[200] = kq[12]                      # a second copy of the same row
+    kq[150] = kq[90]
+    kq[N - 1] = kq[3]                     # the last row
+    kq[250] = kq[0]                       # a copy of the first row
+    kq[301] = kq[300]
+    kq[301, 5] ^= 1                       # one bf16 ulp apart: not a copy
+    kq[310] = kq[305]
+    kq[310, d - 1] ^= 1                   # differs only in the last element
+    kq[320] = 0
+    kq[321] = 0
+    kq[321, 0] = 0x8000                   # -0 against +0 bits: bitwise different
+    for i in range(N):
+        want = next(j for j in range(i + 1) if np.array_equal(kq[j], kq[i]))
+        assert oracle.first_identical(kq, i) == want, i
+    assert [oracle.first_identical(kq, i) for i in (57, 200, 150, N - 1, 250)] == [12, 12, 90, 3, 0]
+    assert oracle.first_identical(kq, 301) == 301 and oracle.first_identical(kq, 310) == 310
+    assert oracle.first_identical(kq, 321) == 321 and oracle.first_identical(kq, 320) == 320
+    assert oracle.first_identical(kq, 0) == 0
+    assert oracle.first_identical(kq, -1) == -1 and oracle.first_identical(kq, N) == -1
+
+
 def test_scores_in_unit_interval_and_permutation_invariance():
     rng = np.random.default_rng(22)
     keys, emb, tokens = _store(rng, 2500, 48)
