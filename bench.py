@@ -197,6 +197,41 @@ def sclk_under_load(torch, step, seconds=1.5):
     return got.get("mhz")
 
 
+def to_dev(a: np.ndarray, dev="cuda:0"):
+    """A host array as a device tensor (bf16 bit patterns travel as int16)."""
+    import torch
+    a = np.ascontiguousarray(a)
+    if a.dtype == np.uint16:
+        a = a.view(np.int16)
+    return torch.from_numpy(a).to(dev)
+
+
+def build_cache(lc, sp, keys, embs, tokens, capacity=None, max_batch=4096, insert_chunk=1 << 18, d_resp=None):
+    """A cache filled with the given entries through lacache_insert (embs: one prefix store, or one per model of
+    an ensemble cache when d_resp is given)."""
+    c = lc.LaCache(capacity or max(1, keys.shape[0]), sp.d, sp.k_cap, sp.in_dtype, max_batch, 0, d_resp=d_resp)
+    n = keys.shape[0]
+    for r0 in range(0, n, insert_chunk):
+        r1 = min(n, r0 + insert_chunk)
+        if d_resp is None:
+            first = c.insert(to_dev(keys[r0:r1]), to_dev(embs[r0:r1]), to_dev(tokens[r0:r1]))
+        else:
+            first = c.insert_ensemble(to_dev(keys[r0:r1]), [to_dev(e[r0:r1]) for e in embs], to_dev(tokens[r0:r1]))
+        assert first == r0
+    return c
+
+
+def host_cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def describe(sp, call_b):
     return (f"{sp.name}: N={sp.N:,} cached entries, d={sp.d} bf16 keys and prefix embeddings, k={sp.k} prefix "
             f"tokens, vocab {sp.vocab}, B={call_b} queries per call "
@@ -205,13 +240,12 @@ def describe(sp, call_b):
 
 
 def run_workload(name, steps, warmup, lc, torch, synth, traffic_db, want_cpu):
-    from tests.gpu_util import gpu_cache, to_dev
     sp = synth.spec(name)
     call_b = synth.SERVE_SMALL_CALL_B if name == "serve_small" else sp.B
     t0 = time.time()
     w = synth.generate(sp)
     log(f"[bench] {name}: generated in {time.time() - t0:.1f}s")
-    c = gpu_cache(lc, sp, w.keys, w.emb, w.tokens, max_batch=max(call_b, 16), insert_chunk=1 << 18)
+    c = build_cache(lc, sp, w.keys, w.emb, w.tokens, max_batch=max(call_b, 16))
     q, a = to_dev(w.queries), to_dev(w.la_emb)
     t = to_dev(np.ascontiguousarray(w.la_tok[:, :sp.k]))
     n_calls = sp.B // call_b
@@ -228,6 +262,9 @@ def run_workload(name, steps, warmup, lc, torch, synth, traffic_db, want_cpu):
     for i in range(warmup):
         step(i)
     torch.cuda.synchronize()
+    # the timed steps, with the library's own events around each stage-1 launch on the call's stream (the stage-1
+    # kernel time of the roofline comes from these very steps)
+    c.profile(True)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
     for i in range(steps):
@@ -235,6 +272,9 @@ def run_workload(name, steps, warmup, lc, torch, synth, traffic_db, want_cpu):
     e1.record()
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / steps
+    k_ms, k_n = c.profile_read()
+    c.profile(False)
+    k_avg = k_ms / max(k_n, 1)
     # per-call times (median and minimum) from a pass with events around every call
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
     for i in range(steps):
@@ -245,14 +285,6 @@ def run_workload(name, steps, warmup, lc, torch, synth, traffic_db, want_cpu):
     per_call = sorted(a.elapsed_time(b) for a, b in ev)
     call_ms = dict(median=per_call[len(per_call) // 2], min=per_call[0])
     sclk = sclk_under_load(torch, step)
-    # a second pass of the same steps with the library's stage-1 events on
-    c.profile(True)
-    for i in range(steps):
-        step(i)
-    torch.cuda.synchronize()
-    k_ms, k_n = c.profile_read()
-    c.profile(False)
-    k_avg = k_ms / max(k_n, 1)
 
     # one more pass over every call of the pool, then the decisions of all its queries
     # (synthetic analogues of the paper's benign and attack hit rates)
@@ -308,7 +340,6 @@ def run_ensemble(steps, warmup, lc, torch, synth):
     1024 / 384 / 768 / 1024, each at the threshold min(0.70, P10) of Appendix A.2, which is 0.70 for the
     synthetic benign prefix cosines U[0.70, 0.98]); half of the benign queries carry one substituted token,
     so the embedding checks decide them."""
-    from tests.gpu_util import gpu_ensemble_cache, to_dev
     sp = synth.spec("serve_large")
     dims = synth.ENSEMBLE_DIMS
     tau_r = (0.70,) * len(dims)
@@ -319,7 +350,7 @@ def run_ensemble(steps, warmup, lc, torch, synth):
     las, la_tok = synth.ensemble_lookahead(sp, dims, embs, w.tokens,
                                            dict(cls=w.cls, target=w.target, la_tok=w.la_tok))
     log(f"[bench] ensemble: generated in {time.time() - t0:.1f}s")
-    c = gpu_ensemble_cache(lc, sp, dims, w.keys, embs, w.tokens, max_batch=call_b, insert_chunk=1 << 18)
+    c = build_cache(lc, sp, w.keys, embs, w.tokens, max_batch=call_b, d_resp=tuple(dims))
     del embs
     q = to_dev(w.queries)
     a = [to_dev(x) for x in las]
@@ -359,7 +390,6 @@ def run_calibration(steps, warmup, lc, torch, synth):
     """Threshold calibration (Appendix A.2) over a million benign pairs at d = 1024 (BGE's dimension):
     pair cosines as the lookup computes them, then tau_c = min(0.80, P5).  One step is one
     lacache_calibrate call; the pair-cosine pass reads 2 * n * d * 2 bytes."""
-    from tests.gpu_util import to_dev
     n, d = 1_000_000, 1024
     t0 = time.time()
     a, b = synth.calibration_pairs(n, d, 0.80, 0.99, seed=66)
@@ -393,7 +423,6 @@ def run_accept(steps, warmup, lc, torch, synth):
     """Speculative-decoding acceptance (Section 4.3) for 256 missed or rejected queries with k = 20 draft
     tokens over a 128,256-token vocabulary: the target's bf16 logits at the 20 positions (1.31 GB) are read
     once; one step is one lacache_accept_length call."""
-    from tests.gpu_util import to_dev
     B, k, V = 256, 20, 128256
     t0 = time.time()
     lg, tok, pd = synth.draft_verification(B, k, V, seed=12)
@@ -426,13 +455,12 @@ def run_lsh(steps, warmup, lc, torch, synth):
     (Eq. (1)): 256 random-hyperplane bits per entry, candidates within 64 differing bits, exact re-rank.
     One step is one lacache_lookup_lsh call; recall is measured over the whole 4096-query pool against the
     exact lookup of the same pool."""
-    from tests.gpu_util import gpu_cache, to_dev
     sp = synth.spec("serve_small")
     call_b, bits, radius = synth.SERVE_SMALL_CALL_B, 256, 64
     t0 = time.time()
     w = synth.generate(sp)
     log(f"[bench] lsh: generated in {time.time() - t0:.1f}s")
-    c = gpu_cache(lc, sp, w.keys, w.emb, w.tokens, max_batch=sp.B, insert_chunk=1 << 18)
+    c = build_cache(lc, sp, w.keys, w.emb, w.tokens, max_batch=sp.B)
     q, a = to_dev(w.queries), to_dev(w.la_emb)
     t = to_dev(np.ascontiguousarray(w.la_tok[:, :sp.k]))
     exact = c.lookup(q, a, t, sp.tau_q, sp.tau_r, sp.k)
@@ -504,13 +532,11 @@ def run_large_interleaved(lc, torch, synth, epochs=8, per_epoch=8, batch=4096):
     lookup and insert of the schedule is in the timed region (inputs resident in HBM beforehand);
     `value` is queries served per second over the whole cycle.  The stage-1 kernel time comes from a
     profiled pass of 8 more lookups at the final size."""
-    from tests.gpu_util import gpu_cache, to_dev
     sp = synth.spec("large")
     total = sp.N + epochs * batch
     t0 = time.time()
     keys, emb, tok = synth.entries(sp, 0, total)
-    c = gpu_cache(lc, sp, keys[:sp.N], emb[:sp.N], tok[:sp.N], capacity=total, max_batch=sp.B,
-                  insert_chunk=1 << 18)
+    c = build_cache(lc, sp, keys[:sp.N], emb[:sp.N], tok[:sp.N], capacity=total, max_batch=sp.B)
     ins, pools = [], []
     for e in range(epochs):
         n = sp.N + e * batch
@@ -536,6 +562,7 @@ def run_large_interleaved(lc, torch, synth, epochs=8, per_epoch=8, batch=4096):
         lookup(0, j)
     torch.cuda.synchronize()
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(epochs)]
+    c.profile(True)
     for e in range(epochs):
         ev[e][0].record()
         for j in range(per_epoch):
@@ -545,6 +572,8 @@ def run_large_interleaved(lc, torch, synth, epochs=8, per_epoch=8, batch=4096):
         assert first == sp.N + e * batch
         ev[e][2].record()
     torch.cuda.synchronize()
+    k_ms, k_n = c.profile_read()
+    c.profile(False)
     total_ms = ev[0][0].elapsed_time(ev[-1][2])
     lookup_ms = sum(ev[e][0].elapsed_time(ev[e][1]) for e in range(epochs))
     insert_ms = sum(ev[e][1].elapsed_time(ev[e][2]) for e in range(epochs))
@@ -565,15 +594,12 @@ def run_large_interleaved(lc, torch, synth, epochs=8, per_epoch=8, batch=4096):
                  latest_batch_found=float(np.mean(served[aimed] & (idx[aimed] == target[aimed]))),
                  latest_batch_queries=int(aimed.sum()))
 
-    c.profile(True)
-    for j in range(per_epoch):
-        lookup(epochs - 1, j)
-    torch.cuda.synchronize()
-    k_ms, k_n = c.profile_read()
-    c.profile(False)
-    k_avg = k_ms / max(k_n, 1)
+    assert k_n == n_lookups
+    k_avg = k_ms / k_n
     n_final = sp.N + epochs * batch
-    achieved = 2.0 * sp.B * n_final * sp.d / (k_avg * 1e-3) / 1e12
+    # the lookups of epoch e search sp.N + e * batch entries
+    flops = sum(per_epoch * 2.0 * sp.B * (sp.N + e * batch) * sp.d for e in range(epochs))
+    achieved = flops / (k_ms * 1e-3) / 1e12
     c.close()
     del pools, ins, outs
     torch.cuda.empty_cache()
@@ -595,10 +621,9 @@ def run_sweep(steps, warmup, lc, torch, synth):
     queries, the LSH path (256 bits, radius 64); then, for 160-256 queries, the exact path with the
     streaming kernel forced (three and four query groups, `set_small_batch(256)`) and, for 128-256, with the
     GEMM kernel forced (`set_small_batch(0)`): the measurements behind the default crossover.  Prints one JSON line per batch size and path set."""
-    from tests.gpu_util import gpu_cache, to_dev
     sp = synth.spec("serve_large")
     w = synth.generate(sp)
-    c = gpu_cache(lc, sp, w.keys, w.emb, w.tokens, max_batch=sp.B, insert_chunk=1 << 18)
+    c = build_cache(lc, sp, w.keys, w.emb, w.tokens, max_batch=sp.B)
     c.enable_lsh(256, to_dev(synth.hyperplanes(256, sp.d, seed=sp.seed + 1000)), 256)
     q, a = to_dev(w.queries), to_dev(w.la_emb)
     t = to_dev(np.ascontiguousarray(w.la_tok[:, :sp.k]))
@@ -682,7 +707,7 @@ def cpu_baseline(sp, w, call_b):
         el1 = time.perf_counter() - t0
     finally:
         oracle.set_num_threads(threads)
-    return dict(value=n / el, unit="lookups/s", cores=threads, kind="oracle",
+    return dict(value=n / el, unit="lookups/s", cores=threads, kind="oracle", cpu_model=host_cpu_model(),
                 sample=f"{n} queries of the same pool against all {sp.N:,} entries (queries quantised outside the "
                        f"timed call; store quantisation {t_store:.1f}s not counted), {el:.1f}s",
                 single_thread=dict(value=n1 / el1, unit="lookups/s", cores=1,

@@ -432,6 +432,30 @@ def test_errors_with_live_handle(lc):
     c.close()
 
 
+def test_create_out_of_memory(lc):
+    """A store that no device can hold (the largest capacity at d = 16384: about 70 TB of keys) is refused with
+    ENOMEM; so is an ensemble whose last prefix store does not fit, with the stores allocated before it
+    released; the device still serves a cache created afterwards."""
+    import torch
+    cap = (1 << 31) - 512
+    with pytest.raises(lc.LaCacheError) as e:
+        lc.LaCache(cap, 16384, 4, oracle.BF16, 16, 0)
+    assert e.value.code == lc.ENOMEM
+    # an ensemble whose second prefix store cannot be allocated (134M x 16384 bf16) after its keys and first
+    # prefix store (32 GB each) were: those are released again
+    free0 = torch.cuda.mem_get_info(0)[0]
+    with pytest.raises(lc.LaCacheError) as e:
+        lc.LaCache(1 << 27, 128, 4, oracle.BF16, 16, 0, d_resp=(128, 16384))
+    assert e.value.code == lc.ENOMEM
+    c = lc.LaCache(1000, 64, 4, oracle.F32, 16, 0)
+    x = torch.randn(10, 64, device="cuda")
+    assert c.insert(x, x, torch.zeros(10, 4, dtype=torch.int32, device="cuda")) == 0
+    idx, score, _, _ = c.lookup(x, x, torch.zeros(10, 4, dtype=torch.int32, device="cuda"), 0.5, 0.5, 4)
+    assert torch.equal(idx.cpu(), torch.arange(10, dtype=torch.int32))
+    c.close()
+    assert abs(torch.cuda.mem_get_info(0)[0] - free0) < (64 << 20)
+
+
 LARGE_STEPS, LARGE_BATCH = 3, 4096
 
 
