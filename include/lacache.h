@@ -285,10 +285,12 @@ int lacache_export_signatures(lacache_t h, int64_t first, int32_t n, uint32_t *s
  * bandwidth-bound streaming kernel, larger ones the matrix-core GEMM kernel.
  * The streaming kernel runs up to four groups of 64 queries (fewer queries
  * per group for d > 1152); 0 <= b_small <= its largest batch, 256 for
- * d <= 1152, else EINVAL.  The default is three groups (192 queries for
- * d <= 1152): from four groups on each CU's share of the contraction, not
- * the key reads, limits the streaming kernel and the GEMM kernel is
- * faster.  0 sends every batch to the GEMM kernel.  Both kernels give the
+ * d <= 1152, else EINVAL.  0 sends every batch to the GEMM kernel.  -1 (the
+ * default) lets each call choose from the number of stored entries n and
+ * the padded dimension d_pad: one query group when n * d_pad >= 2^29, two
+ * when n * d_pad >= 2^27, three below that.  Each added group costs the
+ * streaming kernel a share of the contraction on every CU, so the more keys
+ * there are, the sooner the GEMM kernel is faster.  Both kernels give the
  * same results up to float32 summation order.
  */
 int lacache_set_small_batch(lacache_t h, int32_t b_small);

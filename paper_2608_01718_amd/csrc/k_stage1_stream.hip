@@ -192,10 +192,4 @@ hipError_t launch_stage1_stream(const uint16_t* keys, const uint16_t* qt, int B,
 // Largest batch the streaming kernel takes for d_pad columns.
 int stream_max_batch(int d_pad) { return kStreamMaxGroups * 16 * stream_max_qg(d_pad); }
 
-// Default crossover: three query groups.  Measured on 1M x 768 keys (per call): two groups 0.31 ms, three
-// 0.40 ms, four 0.47-0.48 ms; the GEMM kernel, which pads to one 256-query tile, 0.42 ms for 128-192
-// queries and 0.44 ms for 224-256.  Past two groups each CU's share of the contraction, not the key reads,
-// sets the streaming kernel's time.
-int stream_default_batch(int d_pad) { return 3 * 16 * stream_max_qg(d_pad); }
-
 }  // namespace lacache

@@ -14,8 +14,21 @@
 namespace lacache {
 int stream_max_qg(int d_pad);
 int stream_max_batch(int d_pad);
-int stream_default_batch(int d_pad);
+
+// Default crossover, from per-call times of both kernels for 64-256 queries on random bf16 keys:
+// - 1M x 768, 1M x 1024 and 500k x 2048 keys: the GEMM kernel wins as soon as a second query group is
+//   needed (by 3-6 % against two groups, up to 24 % against three or four);
+// - 300k x 1536: two streaming groups still win (by 6 %), three lose (by 24 %);
+// - 100k x 768: three streaming groups win (by 11-15 %), four lose.
+// Each added group costs the streaming kernel a share of the contraction on every CU, while the GEMM
+// kernel's time for one or two query tiles is its pass over the keys; the fewer the keys, the longer the
+// streaming kernel stays ahead.
+int stream_auto_batch(int d_pad, int64_t n_rows) {
+    const int64_t elems = n_rows * (int64_t)d_pad;
+    const int groups = elems >= (int64_t(1) << 29) ? 1 : elems >= (int64_t(1) << 27) ? 2 : 3;
+    return groups * 16 * stream_max_qg(d_pad);
 }
+}  // namespace lacache
 
 using namespace lacache;
 
@@ -23,7 +36,7 @@ struct lacache_s {
     int device = 0;
     int64_t cap = 0, cap_pad = 0, size = 0;
     int d = 0, d_pad = 0, k_cap = 0, dtype = 0, max_batch = 0, mb_pad = 0;
-    int num_cu = 0, b_small = 128;
+    int num_cu = 0, b_small = -1;  // -1: the crossover follows the cache size (stream_auto_batch)
     int m = 1;                 // prefix models (lookahead checks) per entry
     int d_resp[kMaxModels] = {}, d_pad_resp[kMaxModels] = {};
     uint16_t* keys = nullptr;  // tiled [cap_pad][d_pad]: whole GEMM key tiles plus one spare tile of zero rows
@@ -165,7 +178,7 @@ int lacache_create_ensemble(lacache_t* out, int64_t capacity, int32_t d, int32_t
         return LACACHE_EHIP;
     }
     h->num_cu = prop.multiProcessorCount;
-    h->b_small = stream_default_batch(h->d_pad);
+    h->b_small = -1;
 
     int rc = LACACHE_OK;
     if (rc == LACACHE_OK) rc = alloc_zero((void**)&h->keys, (size_t)h->cap_pad * h->d_pad * 2);
@@ -246,7 +259,7 @@ static int lookup_chunk(lacache_t h, const char* queries, const PrefixModels& mo
                         float tau_q, int k, int32_t* idx, float* score, float* resp, int32_t* dec, hipStream_t s) {
     const int n_rows = (int)h->size;
     int P = 0;
-    const bool small = B <= h->b_small;
+    const bool small = B <= (h->b_small >= 0 ? h->b_small : stream_auto_batch(h->d_pad, n_rows));
     if (n_rows > 0) {
         // the streaming kernel runs more than one query group on whole groups of 16 * stream_max_qg rows
         const int64_t grp = 16 * (int64_t)stream_max_qg(h->d_pad);
@@ -475,7 +488,7 @@ int lacache_replay_fallbacks(lacache_t h, int64_t* count) {
 }
 
 int lacache_set_small_batch(lacache_t h, int32_t b_small) {
-    if (!h || b_small < 0 || b_small > stream_max_batch(h->d_pad)) return LACACHE_EINVAL;
+    if (!h || b_small < -1 || b_small > stream_max_batch(h->d_pad)) return LACACHE_EINVAL;
     h->b_small = b_small;
     return LACACHE_OK;
 }

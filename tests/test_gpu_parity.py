@@ -225,7 +225,8 @@ def _edge(lc, N, d, B, k_cap, k, dtype=oracle.F32, seed=0, b_small=None, neg=Fal
     return w, g, o
 
 
-# b_small None keeps the default crossover (three streaming query groups, 192 queries for d <= 1152)
+# b_small None keeps the default crossover, which for caches this small (n * d_pad < 2^27) is three streaming
+# query groups, 192 queries for d <= 1152
 @pytest.mark.parametrize("N,d,B,k_cap,k,b_small", [
     (1, 64, 5, 1, 1, None),          # a single entry
     (17, 64, 16, 8, 8, None),        # one live row in the last 16-row group
@@ -420,6 +421,9 @@ def test_errors_with_live_handle(lc):
         c.lookup(q, q, t[:4], 0.5, float("inf"), 4)
     with pytest.raises(lc.LaCacheError):
         c.set_small_batch(257)
+    with pytest.raises(lc.LaCacheError):
+        c.set_small_batch(-2)
+    c.set_small_batch(-1)  # back to the size-dependent default
     with pytest.raises(ValueError):
         c.lookup(q.double(), q, t[:4], 0.5, 0.5, 4)
     # a lookup with more queries than max_batch runs in chunks and matches chunk-by-chunk lookups
@@ -441,19 +445,29 @@ def test_create_out_of_memory(lc):
     with pytest.raises(lc.LaCacheError) as e:
         lc.LaCache(cap, 16384, 4, oracle.BF16, 16, 0)
     assert e.value.code == lc.ENOMEM
+
+    def serve_small_cache():
+        c = lc.LaCache(1000, 64, 4, oracle.F32, 16, 0)
+        x = torch.randn(10, 64, device="cuda")
+        tok = torch.zeros(10, 4, dtype=torch.int32, device="cuda")
+        assert c.insert(x, x, tok) == 0
+        idx, _, _, _ = c.lookup(x, x, tok, 0.5, 0.5, 4)
+        assert torch.equal(idx.cpu(), torch.arange(10, dtype=torch.int32))
+        c.close()
+
+    # the first use loads the library's kernels and fills torch's allocator pool: the device memory before and
+    # after the failed create is compared only after that
+    serve_small_cache()
+    torch.cuda.synchronize()
+    free0 = torch.cuda.mem_get_info(0)[0]
     # an ensemble whose second prefix store cannot be allocated (134M x 16384 bf16) after its keys and first
     # prefix store (32 GB each) were: those are released again
-    free0 = torch.cuda.mem_get_info(0)[0]
     with pytest.raises(lc.LaCacheError) as e:
         lc.LaCache(1 << 27, 128, 4, oracle.BF16, 16, 0, d_resp=(128, 16384))
     assert e.value.code == lc.ENOMEM
-    c = lc.LaCache(1000, 64, 4, oracle.F32, 16, 0)
-    x = torch.randn(10, 64, device="cuda")
-    assert c.insert(x, x, torch.zeros(10, 4, dtype=torch.int32, device="cuda")) == 0
-    idx, score, _, _ = c.lookup(x, x, torch.zeros(10, 4, dtype=torch.int32, device="cuda"), 0.5, 0.5, 4)
-    assert torch.equal(idx.cpu(), torch.arange(10, dtype=torch.int32))
-    c.close()
+    torch.cuda.synchronize()
     assert abs(torch.cuda.mem_get_info(0)[0] - free0) < (64 << 20)
+    serve_small_cache()
 
 
 LARGE_STEPS, LARGE_BATCH = 3, 4096
