@@ -269,9 +269,11 @@ def run_workload(name, steps, warmup, lc, torch, synth, traffic_db, want_cpu):
     for i in range(warmup):
         step(i)
     torch.cuda.synchronize()
-    # the timed steps, with the library's own events around each stage-1 launch on the call's stream (the stage-1
-    # kernel time of the roofline comes from these very steps)
-    c.profile(True)
+    # the timed steps; the library times the stage-1 launches of these very steps with HIP events taken from the
+    # kernel's own dispatch on the call's stream (the roofline's kernel time).  Calls of a few hundred
+    # microseconds or less time every tenth launch: a timed launch costs the host ~15 us more, which would weigh
+    # on the throughput measured in the same loop
+    c.profile(1 if call_b >= 1024 else 10)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
     for i in range(steps):

@@ -296,13 +296,20 @@ int lacache_export_signatures(lacache_t h, int64_t first, int32_t n, uint32_t *s
 int lacache_set_small_batch(lacache_t h, int32_t b_small);
 
 /*
- * Timing of the stage-1 kernel.  While enabled, every lookup records a HIP
- * event pair on its stream around its stage-1 launches.  profile_read waits
- * for those events, returns the total elapsed milliseconds and the number of
- * lookups timed (host pointers), and clears the record.  Enabling or
- * disabling also clears it.
+ * Timing of the stage-1 kernel.  With every = n > 0, the 1st, (n+1)-th,
+ * (2n+1)-th ... stage-1 launch from now on (one per lookup, or per chunk of
+ * max_batch queries) is timed: the launch goes through hipExtLaunchKernel
+ * with a HIP event pair that takes the kernel's own start and end times, on
+ * the lookup's stream.  every = 0 stops timing.  profile_read waits for
+ * those events, returns the total elapsed milliseconds and the number of
+ * launches timed (host pointers), and clears the record; calling
+ * lacache_profile also clears it.  The events are created here (256 pairs,
+ * more only when a window outgrows them) and reused.  Timing every launch
+ * costs a few microseconds per lookup, which matters only for lookups that
+ * take tens of microseconds; sampling every n-th launch spreads that cost.
+ * Errors: EINVAL for a null handle or pointer or every < 0, EHIP.
  */
-int lacache_profile(lacache_t h, int32_t enable);
+int lacache_profile(lacache_t h, int32_t every);
 int lacache_profile_read(lacache_t h, double *stage1_ms, int64_t *lookups);
 
 /*

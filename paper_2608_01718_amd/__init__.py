@@ -171,8 +171,8 @@ class LaCache:
     def set_small_batch(self, b_small: int) -> None:
         lacache_set_small_batch(self, b_small)
 
-    def profile(self, enable: bool) -> None:
-        lacache_profile(self, enable)
+    def profile(self, every) -> None:
+        lacache_profile(self, every)
 
     def profile_read(self):
         return lacache_profile_read(self)
@@ -422,12 +422,14 @@ def lacache_set_small_batch(c: LaCache, b_small: int) -> None:
     _check(_lib.lacache_set_small_batch(c.handle, b_small), "lacache_set_small_batch")
 
 
-def lacache_profile(c: LaCache, enable: bool) -> None:
-    _check(_lib.lacache_profile(c.handle, 1 if enable else 0), "lacache_profile")
+def lacache_profile(c: LaCache, every) -> None:
+    """Time every `every`-th stage-1 launch from now on (True: every launch; False or 0: stop)."""
+    n = int(every)  # True -> 1, False -> 0
+    _check(_lib.lacache_profile(c.handle, n), "lacache_profile")
 
 
 def lacache_profile_read(c: LaCache):
-    """(total stage-1 milliseconds, number of lookups timed) since profiling was enabled or last read."""
+    """(total stage-1 milliseconds, number of launches timed) since profiling was enabled or last read."""
     ms, n = ctypes.c_double(0), _i64(0)
     _check(_lib.lacache_profile_read(c.handle, ctypes.byref(ms), ctypes.byref(n)), "lacache_profile_read")
     return ms.value, n.value

@@ -300,7 +300,7 @@ __global__ __launch_bounds__(kWK * 64, 1) void k_stage1_gemm(const u32x4* __rest
 }
 
 hipError_t launch_stage1_gemm(const uint16_t* keys, const uint16_t* qt, int B, int n_rows, int d_pad, uint64_t* part,
-                              int num_cu, int* P_out, hipStream_t s) {
+                              int num_cu, int* P_out, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
     const int kc = d_pad / 32;
     if (n_rows <= 0 || B <= 0 || kc % kU != 0) return hipErrorInvalidValue;
     const int n_qtiles = (B + kTQ - 1) / kTQ;
@@ -330,9 +330,8 @@ hipError_t launch_stage1_gemm(const uint16_t* keys, const uint16_t* qt, int B, i
     static std::atomic<uint64_t> lds_done{0};
     hipError_t e = allow_dynamic_lds((const void*)k_stage1_gemm, kLds, lds_done);
     if (e != hipSuccess) return e;
-    k_stage1_gemm<<<dim3(n_qtiles * n_ranges), dim3(kWK * 64), kLds, s>>>(
-        (const u32x4*)keys, (const u32x4*)qt, kc, n_rows, n_ktiles, n_qtiles, n_ranges, xq, B, n_ranges, part);
-    return hipGetLastError();
+    return launch_timed(k_stage1_gemm, dim3(n_qtiles * n_ranges), dim3(kWK * 64), kLds, s, e0, e1, (const u32x4*)keys,
+                        (const u32x4*)qt, kc, n_rows, n_ktiles, n_qtiles, n_ranges, xq, B, n_ranges, part);
 }
 
 }  // namespace lacache

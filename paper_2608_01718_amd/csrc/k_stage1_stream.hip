@@ -130,14 +130,13 @@ __global__ __launch_bounds__(1024) void k_stage1_stream(const u32x4* __restrict_
 
 template <int QG, bool NT>
 static hipError_t launch_qg(const u32x4* keys, const u32x4* qt, int kc, int groups, int n_rows, int n_ranges,
-                            int n_qgroups, int B, uint64_t* part, hipStream_t s) {
+                            int n_qgroups, int B, uint64_t* part, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
     const size_t lds = (size_t)QG * kc * 1024 + (size_t)kStreamWaves * QG * 16 * 8;
     static std::atomic<uint64_t> lds_allowed{0};
     const hipError_t e = allow_dynamic_lds((const void*)k_stage1_stream<QG, NT>, 160 * 1024, lds_allowed);
     if (e != hipSuccess) return e;
-    k_stage1_stream<QG, NT><<<dim3(n_ranges * n_qgroups), dim3(kStreamWaves * 64), lds, s>>>(
-        keys, qt, kc, groups, n_rows, n_ranges, n_qgroups, B, part);
-    return hipGetLastError();
+    return launch_timed(k_stage1_stream<QG, NT>, dim3(n_ranges * n_qgroups), dim3(kStreamWaves * 64), lds, s, e0, e1,
+                        keys, qt, kc, groups, n_rows, n_ranges, n_qgroups, B, part);
 }
 
 // Largest query-group count QG (16 queries each, at most 4) whose query
@@ -150,7 +149,7 @@ int stream_max_qg(int d_pad) {
 }
 
 hipError_t launch_stage1_stream(const uint16_t* keys, const uint16_t* qt, int B, int n_rows, int d_pad,
-                                uint64_t* part, int num_cu, int* P_out, hipStream_t s) {
+                                uint64_t* part, int num_cu, int* P_out, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
     const int kc = d_pad / 32;
     const int groups = (n_rows + 15) / 16;
     const int maxqg = stream_max_qg(d_pad);
@@ -175,17 +174,21 @@ hipError_t launch_stage1_stream(const uint16_t* keys, const uint16_t* qt, int B,
     const u32x4* q4 = (const u32x4*)qt;
     switch (qg) {
         case 1:
-            return n_qgroups == 1 ? launch_qg<1, true>(k4, q4, kc, groups, n_rows, n_ranges, n_qgroups, B, part, s)
-                                  : launch_qg<1, false>(k4, q4, kc, groups, n_rows, n_ranges, n_qgroups, B, part, s);
+            return n_qgroups == 1
+                       ? launch_qg<1, true>(k4, q4, kc, groups, n_rows, n_ranges, n_qgroups, B, part, s, e0, e1)
+                       : launch_qg<1, false>(k4, q4, kc, groups, n_rows, n_ranges, n_qgroups, B, part, s, e0, e1);
         case 2:
-            return n_qgroups == 1 ? launch_qg<2, true>(k4, q4, kc, groups, n_rows, n_ranges, n_qgroups, B, part, s)
-                                  : launch_qg<2, false>(k4, q4, kc, groups, n_rows, n_ranges, n_qgroups, B, part, s);
+            return n_qgroups == 1
+                       ? launch_qg<2, true>(k4, q4, kc, groups, n_rows, n_ranges, n_qgroups, B, part, s, e0, e1)
+                       : launch_qg<2, false>(k4, q4, kc, groups, n_rows, n_ranges, n_qgroups, B, part, s, e0, e1);
         case 3:
-            return n_qgroups == 1 ? launch_qg<3, true>(k4, q4, kc, groups, n_rows, n_ranges, n_qgroups, B, part, s)
-                                  : launch_qg<3, false>(k4, q4, kc, groups, n_rows, n_ranges, n_qgroups, B, part, s);
+            return n_qgroups == 1
+                       ? launch_qg<3, true>(k4, q4, kc, groups, n_rows, n_ranges, n_qgroups, B, part, s, e0, e1)
+                       : launch_qg<3, false>(k4, q4, kc, groups, n_rows, n_ranges, n_qgroups, B, part, s, e0, e1);
         default:
-            return n_qgroups == 1 ? launch_qg<4, true>(k4, q4, kc, groups, n_rows, n_ranges, n_qgroups, B, part, s)
-                                  : launch_qg<4, false>(k4, q4, kc, groups, n_rows, n_ranges, n_qgroups, B, part, s);
+            return n_qgroups == 1
+                       ? launch_qg<4, true>(k4, q4, kc, groups, n_rows, n_ranges, n_qgroups, B, part, s, e0, e1)
+                       : launch_qg<4, false>(k4, q4, kc, groups, n_rows, n_ranges, n_qgroups, B, part, s, e0, e1);
     }
 }
 

@@ -53,8 +53,12 @@ struct lacache_s {
     uint32_t* sigq = nullptr;      // [max_batch][lsh_bits / 32]
     uint32_t* lsh_cnt = nullptr;   // [max_batch]
     int32_t* lsh_cand = nullptr;   // [max_batch][lsh_max_cand]
-    bool profiling = false;
+    int prof_every = 0;        // lacache_profile: time every prof_every-th stage-1 launch (0: off)
+    uint64_t prof_tick = 0;    // stage-1 launches since profiling was enabled
+    // event pairs of the timed stage-1 launches: created when profiling is enabled (more only if a window
+    // outgrows them) and reused across windows, so a timed lookup only records two events
     std::vector<std::pair<hipEvent_t, hipEvent_t>> prof;
+    size_t prof_used = 0;
 };
 
 namespace {
@@ -114,12 +118,20 @@ int alloc_zero(void** p, size_t bytes) {
     return hipMemset(*p, 0, bytes) == hipSuccess ? LACACHE_OK : LACACHE_EHIP;
 }
 
-void clear_prof(lacache_s* h) {
-    for (auto& p : h->prof) {
-        (void)hipEventDestroy(p.first);
-        (void)hipEventDestroy(p.second);
+void clear_prof(lacache_s* h) { h->prof_used = 0; }
+
+// Makes sure at least n event pairs exist.
+int reserve_prof(lacache_s* h, size_t n) {
+    while (h->prof.size() < n) {
+        hipEvent_t e0 = nullptr, e1 = nullptr;
+        if (hipEventCreate(&e0) != hipSuccess) return LACACHE_EHIP;
+        if (hipEventCreate(&e1) != hipSuccess) {
+            (void)hipEventDestroy(e0);
+            return LACACHE_EHIP;
+        }
+        h->prof.emplace_back(e0, e1);
     }
-    h->prof.clear();
+    return LACACHE_OK;
 }
 
 }  // namespace
@@ -268,15 +280,18 @@ static int lookup_chunk(lacache_t h, const char* queries, const PrefixModels& mo
         if (launch_normalise(queries, h->dtype, B, rows_pad, h->d, h->d_pad, h->qt, 0, true, s) != hipSuccess)
             return LACACHE_EHIP;
         hipEvent_t e0 = nullptr, e1 = nullptr;
-        if (h->profiling) {
-            if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) return LACACHE_EHIP;
-            h->prof.emplace_back(e0, e1);
-            if (hipEventRecord(e0, s) != hipSuccess) return LACACHE_EHIP;
+        if (h->prof_every > 0 && h->prof_tick++ % h->prof_every == 0) {
+            if (h->prof_used == h->prof.size() && reserve_prof(h, 2 * h->prof.size() + 64) != LACACHE_OK)
+                return LACACHE_EHIP;
+            e0 = h->prof[h->prof_used].first;
+            e1 = h->prof[h->prof_used].second;
+            ++h->prof_used;
         }
-        hipError_t e = small ? launch_stage1_stream(h->keys, h->qt, B, n_rows, h->d_pad, h->part, h->num_cu, &P, s)
-                             : launch_stage1_gemm(h->keys, h->qt, B, n_rows, h->d_pad, h->part, h->num_cu, &P, s);
+        // with profiling on, the events take the stage-1 kernel's own start and end times (launch_timed)
+        hipError_t e =
+            small ? launch_stage1_stream(h->keys, h->qt, B, n_rows, h->d_pad, h->part, h->num_cu, &P, s, e0, e1)
+                  : launch_stage1_gemm(h->keys, h->qt, B, n_rows, h->d_pad, h->part, h->num_cu, &P, s, e0, e1);
         if (e != hipSuccess) return LACACHE_EHIP;
-        if (h->profiling && hipEventRecord(e1, s) != hipSuccess) return LACACHE_EHIP;
     }
     if (launch_finalize_verify(h->part, P, !small, h->keys, h->qt, B, n_rows, h->dtype, h->d, models, la_tok, k,
                                h->tokens, h->k_cap, tau_q, idx, score, resp, dec, h->fallbacks, s) != hipSuccess)
@@ -493,12 +508,15 @@ int lacache_set_small_batch(lacache_t h, int32_t b_small) {
     return LACACHE_OK;
 }
 
-int lacache_profile(lacache_t h, int32_t enable) {
-    if (!h) return LACACHE_EINVAL;
+int lacache_profile(lacache_t h, int32_t every) {
+    if (!h || every < 0) return LACACHE_EINVAL;
     DeviceGuard g(h->device);
+    if (!g.ok) return LACACHE_EHIP;
     clear_prof(h);
-    h->profiling = enable != 0;
-    return LACACHE_OK;
+    h->prof_every = every;
+    h->prof_tick = 0;
+    // the events of a typical timing window, created now rather than inside it
+    return every > 0 ? reserve_prof(h, 256) : LACACHE_OK;
 }
 
 int lacache_profile_read(lacache_t h, double* stage1_ms, int64_t* lookups) {
@@ -508,7 +526,8 @@ int lacache_profile_read(lacache_t h, double* stage1_ms, int64_t* lookups) {
     double total = 0.0;
     int64_t cnt = 0;
     int rc = LACACHE_OK;
-    for (auto& p : h->prof) {
+    for (size_t i = 0; i < h->prof_used; ++i) {
+        const auto& p = h->prof[i];
         float ms = 0.f;
         if (hipEventSynchronize(p.second) != hipSuccess || hipEventElapsedTime(&ms, p.first, p.second) != hipSuccess) {
             rc = LACACHE_EHIP;

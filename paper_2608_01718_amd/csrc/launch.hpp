@@ -1,10 +1,13 @@
 // launch.hpp -- host-side launchers of the gfx950 kernels (called by the C ABI in lacache.cpp).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 #include <atomic>
+#include <tuple>
+#include <utility>
 
 namespace lacache {
 
@@ -26,6 +29,26 @@ inline hipError_t allow_dynamic_lds(const void* fn, int bytes, std::atomic<uint6
     return e;
 }
 
+// Launch `kernel` on stream s.  With events e0 and e1 (both or neither) the launch goes through
+// hipExtLaunchKernel, which takes the kernel's own start and end times into them from its dispatch: no
+// event packets of their own on the stream, so timing a kernel does not change the gaps around it.
+template <typename... P, typename... A>
+hipError_t launch_timed(void (*kernel)(P...), dim3 grid, dim3 block, size_t lds, hipStream_t s, hipEvent_t e0,
+                        hipEvent_t e1, A... args) {
+    static_assert(sizeof...(P) == sizeof...(A), "one argument per kernel parameter");
+    if (!e0) {
+        kernel<<<grid, block, lds, s>>>(static_cast<P>(args)...);
+        return hipGetLastError();
+    }
+    std::tuple<P...> t{static_cast<P>(args)...};
+    return std::apply(
+        [&](auto&... v) {
+            void* a[] = {(void*)&v...};
+            return hipExtLaunchKernel((const void*)kernel, grid, block, a, lds, s, e0, e1, 0);
+        },
+        t);
+}
+
 // Normalise `rows` input rows (dtype 0 f32 / 1 bf16, row-major [rows][d]) and
 // store them as bfloat16 at destination rows row0 .. row0+rows-1, zero-filling
 // up to rows_pad rows and d_pad columns; `tiled` selects the key layout,
@@ -41,8 +64,10 @@ hipError_t launch_export(const uint16_t* src, int64_t first, int n, int d, int d
 // a multiple of 16, or up to four such groups, zero-padded to whole groups) against n_rows tiled keys.  Writes, for every query b
 // and every workgroup p of the launch, the packed top-1 candidate
 // part[b * P + p] (P <= kMaxPartials).  Returns the number of partials P through *P_out.
+// With events e0 / e1 the kernel's run time is recorded into them (launch_timed).
 hipError_t launch_stage1_stream(const uint16_t* keys, const uint16_t* qt, int B, int n_rows, int d_pad,
-                                uint64_t* part, int num_cu, int* P_out, hipStream_t s);
+                                uint64_t* part, int num_cu, int* P_out, hipStream_t s, hipEvent_t e0 = nullptr,
+                                hipEvent_t e1 = nullptr);
 
 // Stage 1, compute-bound path (matrix-core GEMM with a fused row maximum): queries qt (tiled, rows zero-padded
 // to a multiple of kGemmQueryTile) against n_rows keys.  The key store must hold whole tiles of kGemmKeyTile
@@ -52,7 +77,8 @@ hipError_t launch_stage1_stream(const uint16_t* keys, const uint16_t* qt, int B,
 constexpr int kGemmKeyTile = 512;
 constexpr int kGemmQueryTile = 128;
 hipError_t launch_stage1_gemm(const uint16_t* keys, const uint16_t* qt, int B, int n_rows, int d_pad,
-                              uint64_t* part, int num_cu, int* P_out, hipStream_t s);
+                              uint64_t* part, int num_cu, int* P_out, hipStream_t s, hipEvent_t e0 = nullptr,
+                              hipEvent_t e1 = nullptr);
 
 // The response-prefix embedding models of stage 2 (one per lookahead check of an ensemble).
 constexpr int kMaxModels = 8;

@@ -148,9 +148,12 @@ def test_parity_large_clustered_reduced(lc):
 
 
 def test_parity_serve_small_full_size_sampled(lc):
-    sp = synth.spec("serve_small", B=256)
+    """The 1M x 768 workload in 16-query calls (the streaming kernel) at full size: 1024 queries, 512
+    or more stratified rows of them (every collision query, 256 benign and 256 miss) against the oracle."""
+    sp = synth.spec("serve_small", B=1024)
     w = synth.generate(sp)
-    rows = sample_rows(w.cls, w.target, 48)
+    rows = sample_rows(w.cls, w.target, 768)
+    assert len(rows) >= 512
     _run(lc, sp, w=w, call_b=synth.SERVE_SMALL_CALL_B, rows=rows)
 
 
@@ -433,6 +436,42 @@ def test_errors_with_live_handle(lc):
     parts = [[z.cpu() for z in c.lookup(q2[i:i + 8], q2[i:i + 8], t2[i:i + 8], 0.1, 0.1, 4)] for i in (0, 8, 16)]
     for j in range(4):
         assert torch.equal(whole[j].view(torch.int32), torch.cat([p[j] for p in parts]).view(torch.int32))
+    c.close()
+
+
+def test_profile_times_every_stage1_launch(lc):
+    """lacache_profile: every lookup of a window is timed (streaming and GEMM stage 1 alike), a window longer
+    than the events made at enable time still counts every call, reading clears the window, sampling every
+    n-th launch times exactly those, and lookups made while profiling is off are not counted."""
+    import torch
+    c = lc.LaCache(5000, 256, 4, oracle.BF16, 512, 0)
+    x = torch.randn(5000, 256, device="cuda", dtype=torch.bfloat16)
+    tok = torch.zeros(5000, 4, dtype=torch.int32, device="cuda")
+    c.insert(x, x, tok)
+    q16, q300 = x[:16], x[:300]
+    c.lookup(q16, q16, tok[:16], 0.5, 0.5, 4)
+    c.profile(True)
+    c.lookup(q16, q16, tok[:16], 0.5, 0.5, 4)       # streaming kernel
+    c.lookup(q300, q300, tok[:300], 0.5, 0.5, 4)    # GEMM kernel
+    ms, n = c.profile_read()
+    assert n == 2 and ms > 0
+    ms, n = c.profile_read()
+    assert n == 0 and ms == 0
+    for _ in range(700):                            # more than the event pairs made when profiling was enabled
+        c.lookup(q16, q16, tok[:16], 0.5, 0.5, 4)
+    ms, n = c.profile_read()
+    assert n == 700 and ms > 0
+    c.profile(3)                                    # every third launch: the 1st, 4th, 7th of 8
+    for _ in range(8):
+        c.lookup(q16, q16, tok[:16], 0.5, 0.5, 4)
+    ms, n = c.profile_read()
+    assert n == 3 and ms > 0
+    c.profile(False)
+    c.lookup(q16, q16, tok[:16], 0.5, 0.5, 4)
+    ms, n = c.profile_read()
+    assert n == 0
+    with pytest.raises(lc.LaCacheError):
+        c.profile(-1)
     c.close()
 
 
