@@ -229,14 +229,21 @@ def build_cache(lc, sp, keys, embs, tokens, capacity=None, max_batch=4096, inser
 
 
 def host_cpu_model() -> str:
+    """The host CPU as /proc/cpuinfo names it, with its family / model / stepping numbers (a virtual machine
+    may report only a short name)."""
+    info = {}
     try:
         with open("/proc/cpuinfo") as f:
             for line in f:
-                if line.startswith("model name"):
-                    return line.split(":", 1)[1].strip()
+                if not line.strip():
+                    break  # the first processor's block is enough
+                k, _, v = line.partition(":")
+                info[k.strip()] = v.strip()
     except OSError:
-        pass
-    return "unknown"
+        return "unknown"
+    name = info.get("model name", "unknown")
+    ids = [f"{k} {info[k]}" for k in ("cpu family", "model", "stepping") if k in info]
+    return f"{name} ({', '.join(ids)})" if ids else name
 
 
 def describe(sp, call_b):

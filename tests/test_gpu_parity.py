@@ -319,7 +319,7 @@ def test_near_tie_exemption_exercised(lc, B, b_small):
 
 @pytest.mark.parametrize("B", [64, 100, 128, 200, 256])
 def test_determinism_and_paths_agree(lc, B):
-    """Five repeats give identical outputs, and the streaming and GEMM stage-1 paths give identical outputs."""
+    """Ten repeats give identical outputs, and the streaming and GEMM stage-1 paths give identical outputs."""
     import torch
     sp = synth.spec("mid", N=20_000, B=B)
     w = synth.generate(sp)
