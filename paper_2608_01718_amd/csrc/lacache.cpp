@@ -277,7 +277,9 @@ static int lookup_chunk(lacache_t h, const char* queries, const PrefixModels& mo
         const int64_t grp = 16 * (int64_t)stream_max_qg(h->d_pad);
         const int64_t rows_pad =
             small ? (B <= grp ? round_up(B, 16) : round_up(B, grp)) : round_up(B, kGemmQueryTile);
-        if (launch_normalise(queries, h->dtype, B, rows_pad, h->d, h->d_pad, h->qt, 0, true, s) != hipSuccess)
+        // the streaming kernel normalises its queries itself up to d_pad = 2048; otherwise they are staged
+        const bool fused = small && stream_fused_ncq(h->d_pad) > 0;
+        if (!fused && launch_normalise(queries, h->dtype, B, rows_pad, h->d, h->d_pad, h->qt, 0, true, s) != hipSuccess)
             return LACACHE_EHIP;
         hipEvent_t e0 = nullptr, e1 = nullptr;
         if (h->prof_every > 0 && h->prof_tick++ % h->prof_every == 0) {
@@ -288,9 +290,10 @@ static int lookup_chunk(lacache_t h, const char* queries, const PrefixModels& mo
             ++h->prof_used;
         }
         // with profiling on, the events take the stage-1 kernel's own start and end times (launch_timed)
-        hipError_t e =
-            small ? launch_stage1_stream(h->keys, h->qt, B, n_rows, h->d_pad, h->part, h->num_cu, &P, s, e0, e1)
-                  : launch_stage1_gemm(h->keys, h->qt, B, n_rows, h->d_pad, h->part, h->num_cu, &P, s, e0, e1);
+        hipError_t e = small ? launch_stage1_stream(h->keys, h->qt, B, n_rows, h->d_pad, h->part, h->num_cu, &P, s,
+                                                    e0, e1, fused ? queries : nullptr, h->dtype, h->d)
+                             : launch_stage1_gemm(h->keys, h->qt, B, n_rows, h->d_pad, h->part, h->num_cu, &P, s,
+                                                  e0, e1);
         if (e != hipSuccess) return LACACHE_EHIP;
     }
     if (launch_finalize_verify(h->part, P, !small, h->keys, h->qt, B, n_rows, h->dtype, h->d, models, la_tok, k,

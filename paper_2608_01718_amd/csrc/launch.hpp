@@ -64,10 +64,13 @@ hipError_t launch_export(const uint16_t* src, int64_t first, int n, int d, int d
 // a multiple of 16, or up to four such groups, zero-padded to whole groups) against n_rows tiled keys.  Writes, for every query b
 // and every workgroup p of the launch, the packed top-1 candidate
 // part[b * P + p] (P <= kMaxPartials).  Returns the number of partials P through *P_out.
-// With events e0 / e1 the kernel's run time is recorded into them (launch_timed).
+// With events e0 / e1 the kernel's run time is recorded into them (launch_timed).  With qraw (the caller's
+// [B][d] query rows, dtype 0 f32 / 1 bf16) the kernel normalises the queries itself and qt is not read; this
+// takes d_pad <= 2048 (stream_fused_ncq(d_pad) > 0).
 hipError_t launch_stage1_stream(const uint16_t* keys, const uint16_t* qt, int B, int n_rows, int d_pad,
                                 uint64_t* part, int num_cu, int* P_out, hipStream_t s, hipEvent_t e0 = nullptr,
-                                hipEvent_t e1 = nullptr);
+                                hipEvent_t e1 = nullptr, const void* qraw = nullptr, int dtype = 0, int d = 0);
+int stream_fused_ncq(int d_pad);
 
 // Stage 1, compute-bound path (matrix-core GEMM with a fused row maximum): queries qt (tiled, rows zero-padded
 // to a multiple of kGemmQueryTile) against n_rows keys.  The key store must hold whole tiles of kGemmKeyTile

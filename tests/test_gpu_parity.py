@@ -244,6 +244,7 @@ def _edge(lc, N, d, B, k_cap, k, dtype=oracle.F32, seed=0, b_small=None, neg=Fal
     (900, 1280, 150, 8, 8, 192),     # d > 1152: groups of 48 queries, four of them, the last holding 6
     (4097, 768, 300, 16, 16, None),  # ragged everything on the large-batch path
     (300, 1024, 1, 32, 32, None),    # B = 1
+    (600, 2100, 40, 8, 8, None),     # d_pad > 2048: queries staged by the normaliser, two 32-query groups
 ])
 @pytest.mark.parametrize("dtype", [oracle.F32, oracle.BF16])
 def test_edge_shapes(lc, N, d, B, k_cap, k, b_small, dtype):
