@@ -73,7 +73,7 @@ def parse():
     return ap.parse_args()
 
 
-STAGE1_KERNELS = {"serve_large": "k_stage1_gemm(", "serve_small": "k_stage1_stream<1, true>",
+STAGE1_KERNELS = {"serve_large": "k_stage1_gemm(", "serve_small": "k_stage1_stream<1, true, 2>",
                   "large": "k_stage1_gemm("}
 STAGE1_SOURCES = {"serve_large": ["k_stage1_gemm.hip", "common.hpp"],
                   "serve_small": ["k_stage1_stream.hip", "common.hpp"],
