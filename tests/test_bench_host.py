@@ -39,12 +39,17 @@ def test_pmc_summary_scales_by_the_copy(tmp_path):
               [("copy_kernel", copy_mib * 1024 / 2)])
     _counters(str(root / "write_copy" / "run_counter_collection.csv"), "WRITE_SIZE",
               [("copy_kernel", copy_mib * 1024)])
-    gemm, stream = "lacache::k_stage1_gemm(...)", "void lacache::k_stage1_stream<1, true>(...)"
+    gemm, stream = "lacache::k_stage1_gemm(...)", "void lacache::k_stage1_stream<1, true, 2>(...)"
     _counters(str(root / "fetch_bench" / "run_counter_collection.csv"), "FETCH_SIZE",
               [(gemm, 3.0e6), (gemm, 3.2e6), (gemm, 9.9e9), (stream, 750_000.0), (stream, 750_001.0),
                (stream, 10.0), ("other", 1.0)])
     _counters(str(root / "write_bench" / "run_counter_collection.csv"), "WRITE_SIZE",
               [(gemm, 4700.0), (gemm, 4700.0), (gemm, 4700.0), (stream, 128.0), (stream, 128.0), (stream, 128.0)])
+    # the 4M x 1024 schedule has counter runs of its own (its GEMM launches, and the streaming leg before it)
+    _counters(str(root / "fetch_large" / "run_counter_collection.csv"), "FETCH_SIZE",
+              [(stream, 1.0), (gemm, 5.7e6), (gemm, 5.8e6), (gemm, 5.9e6), (gemm, 5.6e6), (gemm, 6.0e6)])
+    _counters(str(root / "write_large" / "run_counter_collection.csv"), "WRITE_SIZE",
+              [(stream, 1.0), (gemm, 480.0), (gemm, 500.0), (gemm, 490.0), (gemm, 510.0), (gemm, 470.0)])
     out = tmp_path / "traffic.json"
     r = subprocess.run([sys.executable, BENCH, "--pmc-summary", str(root), "--traffic", str(out), "--copy-mib",
                         str(copy_mib)], capture_output=True, text=True, timeout=120)
@@ -57,5 +62,8 @@ def test_pmc_summary_scales_by_the_copy(tmp_path):
     assert d["serve_large"]["traffic_bytes"] == pytest.approx(3.2e6 * 2048 + 4700.0 * 1024)
     assert d["serve_small"]["fetch_bytes"] == pytest.approx(750_000.0 * 1024 * 2)
     assert d["serve_small"]["dispatches"] == 3 and d["serve_large"]["dispatches"] == 3
+    assert d["large"]["fetch_bytes"] == pytest.approx(5.8e6 * 1024 * 2)
+    assert d["large"]["write_bytes"] == pytest.approx(490.0 * 1024)
+    assert d["large"]["dispatches"] == 5
     # each entry carries the digest of the kernel sources it was measured on
     assert len(d["serve_large"]["sources_digest"]) == 16
