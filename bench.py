@@ -15,13 +15,14 @@ same keys with the four-model lookahead ensemble (Section 4.4) under
 (Appendix A.2) under "calibration", and the speculative-decoding acceptance
 of 256 x 20 draft tokens (Section 4.3) under "accept", and the serve_small
 lookup with stage 1 through the LSH index (Eq. (1)) under "lsh".  For
-each, "roofline" rates the stage-1 kernel, timed with HIP events recorded by
-the library on the launch stream, against the MI355X peak (bf16 dense MFMA
-2.5 PFLOP/s, HBM 8 TB/s).  "cpu_baseline" times the CPU oracle on a bounded
-sample of the same workload on the host cores.  "attainable" rates the same
-kernels against what this GPU sustains, measured at start-up by the
-roofline_probe executable built beside the library: v_mfma_f32_32x32x16_bf16
-throughput on random bf16 operands, and a plain streaming read.
+each, "roofline" rates the stage-1 kernel, timed over the timed steps with HIP
+events that the library attaches to the kernel's own dispatch on the launch
+stream, against the MI355X peak (bf16 dense MFMA 2.5 PFLOP/s, HBM 8 TB/s).
+"cpu_baseline" times the CPU oracle on a bounded sample of the same workload
+on the host cores.  "attainable" rates the same kernels against what this GPU
+sustains, measured at start-up by the roofline_probe executable built beside
+the library: bf16 MFMA throughput on random operands (the better of the
+16x16x32 and 32x32x16 forms) and a streaming read.
 """
 from __future__ import annotations
 

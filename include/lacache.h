@@ -284,14 +284,15 @@ int lacache_export_signatures(lacache_t h, int64_t first, int32_t n, uint32_t *s
  * Batch-size crossover of stage 1: batches of at most b_small queries use the
  * bandwidth-bound streaming kernel, larger ones the matrix-core GEMM kernel.
  * The streaming kernel runs up to four groups of 64 queries (fewer queries
- * per group for d > 1152); 0 <= b_small <= its largest batch, 256 for
- * d <= 1152, else EINVAL.  0 sends every batch to the GEMM kernel.  -1 (the
- * default) lets each call choose from the number of stored entries n and
- * the padded dimension d_pad: one query group when n * d_pad >= 2^29, two
- * when n * d_pad >= 2^27, three below that.  Each added group costs the
- * streaming kernel a share of the contraction on every CU, so the more keys
- * there are, the sooner the GEMM kernel is faster.  Both kernels give the
- * same results up to float32 summation order.
+ * per group for d > 1152).  b_small is -1, or from 0 up to the streaming
+ * kernel's largest batch (256 for d <= 1152); anything else is EINVAL.
+ * 0 sends every batch to the GEMM kernel.  -1 (the default) lets each call
+ * choose from the number of stored entries n and the padded dimension d_pad:
+ * one query group when n * d_pad >= 2^29, two when n * d_pad >= 2^27, three
+ * below that.  Each added group costs the streaming kernel a share of the
+ * contraction on every CU, so the more keys there are, the sooner the GEMM
+ * kernel is faster.  Both kernels accumulate every score with the same
+ * matrix instruction sequence, so their results are bit-identical.
  */
 int lacache_set_small_batch(lacache_t h, int32_t b_small);
 

@@ -8,7 +8,6 @@ namespace lacache {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 constexpr int kWave = 64;
@@ -110,12 +109,6 @@ __host__ __device__ inline uint16_t bf16_rne_quotient(float v, double n, float r
 }
 
 __device__ inline float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
-
-// Element j of a row of input vectors as a double (dtype 0 = float32, 1 = bfloat16).
-__device__ inline double load_in(const void* row, int dtype, int j) {
-    if (dtype == 0) return (double)((const float*)row)[j];
-    return (double)bf16_to_f32(((const uint16_t*)row)[j]);
-}
 
 // Elements j0 .. j0+7 of a row as floats (0 beyond d; bfloat16 widens exactly): one or two 16-byte loads when
 // the chunk is whole and 16-byte aligned, element loads otherwise.  The values are the same either way.
@@ -298,10 +291,6 @@ __device__ inline float unpack_score(uint64_t p) { return unorder_f32((uint32_t)
 
 __device__ inline f32x4 mfma16x16x32(u32x4 a, u32x4 b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c,
-                                                   0, 0, 0);
-}
-__device__ inline f32x16 mfma32x32x16(u32x4 a, u32x4 b, f32x16 c) {
-    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c,
                                                    0, 0, 0);
 }
 
