@@ -149,6 +149,13 @@ int lacache_insert_ensemble(lacache_t h, const void *keys, const void *const *re
  * Similarities are dot products of the bfloat16-rounded normalised vectors,
  * accumulated in float32.  B == 0 is a no-op.  Only for a cache with m = 1
  * (else LACACHE_EINVAL).
+ * A lookup (this call and lacache_lookup_ensemble) only enqueues kernels on
+ * the stream: no allocation, memory set, copy or host synchronisation.  It
+ * can therefore be captured into a HIP graph (with profiling off) and
+ * replayed.  A captured lookup keeps what was fixed at capture time: the
+ * argument pointers, B, k, the thresholds, the number of stored entries and
+ * the stage-1 kernel chosen for them.  Entries inserted after the capture
+ * are not searched until the lookup is captured again.
  */
 int lacache_lookup(lacache_t h, const void *queries, const void *lookahead_emb, const int32_t *lookahead_tokens,
                    int32_t B, float tau_q, float tau_r, int32_t k, int32_t *idx, float *score, float *resp_score,

@@ -380,6 +380,60 @@ def test_calls_enqueued_on_side_streams(lc):
         c.close()
 
 
+def test_lookup_graph_capture_and_replay(lc):
+    """Lookups of both stage-1 paths (64 queries on the streaming kernel, 300 on the GEMM kernel) captured into
+    one HIP graph and replayed: the lookup enqueues only kernels, so the capture holds it whole.  Every replay,
+    with new query contents copied into the captured inputs and the outputs overwritten by eager work
+    between replays, equals an eager lookup on the same inputs bit for bit."""
+    import torch
+    sp = synth.spec("mid", N=20_000, B=364)
+    w = synth.generate(sp)
+    c = gpu_cache(lc, sp, w.keys, w.emb, w.tokens)
+    q_all, a_all = to_dev(w.queries), to_dev(w.la_emb)
+    t_all = to_dev(np.ascontiguousarray(w.la_tok[:, :sp.k]))
+    q, a, t = q_all.clone(), a_all.clone(), t_all.clone()
+    calls = ((64, 0), (300, 64))  # (B, first row): streaming path, then GEMM path (n * d_pad < 2^27: 192 stream)
+    dts = (torch.int32, torch.float32, torch.float32, torch.int32)
+    outs = {B: tuple(torch.empty(B, dtype=dt, device="cuda") for dt in dts) for B, _ in calls}
+
+    def run(o):
+        for B, r0 in calls:
+            c.lookup(q[r0:r0 + B], a[r0:r0 + B], t[r0:r0 + B], sp.tau_q, sp.tau_r, sp.k, out=o[B])
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        run(outs)  # first use outside the capture (kernel attributes are set once)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        run(outs)
+    rng = np.random.default_rng(5)
+    for rep in range(4):
+        perm = torch.as_tensor(rng.permutation(sp.B), device="cuda")
+        q.copy_(q_all[perm])
+        a.copy_(a_all[perm])
+        t.copy_(t_all[perm])
+        for o in outs.values():
+            for x in o:
+                x.fill_(-7)
+        graph.replay()
+        torch.cuda.synchronize()
+        got = {B: [x.clone() for x in outs[B]] for B, _ in calls}
+        ref = {B: tuple(torch.empty(B, dtype=dt, device="cuda") for dt in dts) for B, _ in calls}
+        run(ref)
+        torch.cuda.synchronize()
+        for B, _ in calls:
+            for g_, r_ in zip(got[B], ref[B]):
+                gb, rb = g_.cpu().numpy(), r_.cpu().numpy()
+                np.testing.assert_array_equal(gb.view(np.uint32), rb.view(np.uint32), err_msg=f"replay {rep}, B={B}")
+        say(f"[ok] graph replay {rep}: hits {int((ref[300][3] >= 2).sum().item())} of 300")
+    assert c.replay_fallbacks() == 0
+    graph.reset()
+    c.close()
+
+
 def test_interleaved_inserts(lc):
     """A query planted near an entry is a miss before that entry is inserted and a hit after it."""
     sp = synth.spec("large", N=12_288, B=256)
