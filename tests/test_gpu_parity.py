@@ -245,10 +245,32 @@ def _edge(lc, N, d, B, k_cap, k, dtype=oracle.F32, seed=0, b_small=None, neg=Fal
     (4097, 768, 300, 16, 16, None),  # ragged everything on the large-batch path
     (300, 1024, 1, 32, 32, None),    # B = 1
     (600, 2100, 40, 8, 8, None),     # d_pad > 2048: queries staged by the normaliser, two 32-query groups
+    (300, 6000, 40, 8, 8, None),     # d_pad > 4992: no streaming query group fits LDS, every batch on the GEMM
+    (150, 16384, 20, 4, 4, None),    # the largest d a cache takes
 ])
 @pytest.mark.parametrize("dtype", [oracle.F32, oracle.BF16])
 def test_edge_shapes(lc, N, d, B, k_cap, k, b_small, dtype):
     _edge(lc, N, d, B, k_cap, k, dtype, b_small=b_small)
+
+
+def test_crossover_limits_for_wide_rows(lc):
+    """Where not even one 16-query group of the streaming kernel fits LDS (d_pad > 4992), no batch size can be
+    sent to it: setting the crossover above 0 is EINVAL, 0 and -1 are accepted, and lookups run (on the GEMM
+    kernel) either way."""
+    import torch
+    c = lc.LaCache(64, 6000, 4, oracle.F32, 64, 0)
+    x = torch.randn(64, 6000, device="cuda")
+    tok = torch.zeros(64, 4, dtype=torch.int32, device="cuda")
+    c.insert(x, x, tok)
+    with pytest.raises(lc.LaCacheError) as e:
+        c.set_small_batch(16)
+    assert e.value.code == lc.EINVAL
+    for b_small in (0, -1):
+        c.set_small_batch(b_small)
+        idx, score, _, dec = c.lookup(x[:5], x[:5], tok[:5], 0.5, 0.5, 4)
+        assert torch.equal(idx.cpu(), torch.arange(5, dtype=torch.int32))
+        assert torch.all(dec.cpu() == oracle.HIT_EXACT)
+    c.close()
 
 
 @pytest.mark.parametrize("b_small,B", [(0, 40), (64, 40), (128, 100), (256, 200)])
