@@ -247,6 +247,10 @@ def _edge(lc, N, d, B, k_cap, k, dtype=oracle.F32, seed=0, b_small=None, neg=Fal
     (600, 2100, 40, 8, 8, None),     # d_pad > 2048: queries staged by the normaliser, two 32-query groups
     (300, 6000, 40, 8, 8, None),     # d_pad > 4992: no streaming query group fits LDS, every batch on the GEMM
     (150, 16384, 20, 4, 4, None),    # the largest d a cache takes
+    (40, 1, 9, 4, 4, None),          # d = 1: every key normalises to +-1, whole halves of the store tie exactly
+    (40, 1, 200, 4, 4, None),        # the same ties on the GEMM path: the first 16-row group, then its lowest row
+    (3000, 1, 300, 4, 4, None),      # ties spread over six key tiles and several workgroups' ranges
+    (50, 64, 8, 4096, 4096, None),   # k = k_cap = 4096, the largest prefix a cache takes (64 ballot rounds)
 ])
 @pytest.mark.parametrize("dtype", [oracle.F32, oracle.BF16])
 def test_edge_shapes(lc, N, d, B, k_cap, k, b_small, dtype):
@@ -296,6 +300,13 @@ def test_empty_cache(lc):
     idx, score, resp, dec = (x.cpu().numpy() for x in c.lookup(q, q, t, 0.5, 0.5, 4))
     assert np.all(idx == -1) and np.all(np.isnan(score)) and np.all(np.isnan(resp)) and np.all(dec == 0)
     assert np.all(resp.view(np.uint32) == 0x7FC00000)
+    # a lookup of no queries is a no-op, on an empty cache and on a filled one
+    e = c.lookup(q[:0], q[:0], t[:0], 0.5, 0.5, 4)
+    assert all(x.numel() == 0 for x in e)
+    c.insert(q, q, t)
+    e = c.lookup(q[:0], q[:0], t[:0], 0.5, 0.5, 4)
+    assert all(x.numel() == 0 for x in e)
+    torch.cuda.synchronize()
     c.close()
 
 
