@@ -277,8 +277,10 @@ static int lookup_chunk(lacache_t h, const char* queries, const PrefixModels& mo
         const int64_t grp = 16 * (int64_t)stream_max_qg(h->d_pad);
         const int64_t rows_pad =
             small ? (B <= grp ? round_up(B, 16) : round_up(B, grp)) : round_up(B, kGemmQueryTile);
-        // the streaming kernel normalises its queries itself up to d_pad = 2048; otherwise they are staged
-        const bool fused = small && stream_fused_ncq(h->d_pad) > 0;
+        // up to 32 queries (at most two rows per wave) and d_pad = 2048 the streaming kernel normalises its queries
+        // itself, saving the staging launch; with more rows per wave its prologue would cost more than that launch
+        // (64 queries on 10k x 384 keys: ~5.7 us of prologue against ~4 us of staging), so they are staged
+        const bool fused = small && B <= 32 && stream_fused_ncq(h->d_pad) > 0;
         if (!fused && launch_normalise(queries, h->dtype, B, rows_pad, h->d, h->d_pad, h->qt, 0, true, s) != hipSuccess)
             return LACACHE_EHIP;
         hipEvent_t e0 = nullptr, e1 = nullptr;
